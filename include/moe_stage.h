@@ -1,0 +1,201 @@
+/*
+ * moe_stage.h - C ABI of the MI355X (gfx950) MoE expert stage.
+ *
+ * The stage is the data-parallel work one device runs on its own share of the
+ * experts of a MoE layer in a disaggregated attention/MoE prefill system
+ * (paper: "ASAP: A Disaggregated and Asynchronous Inference System for MoE
+ * Prefill", sections 3.2 and 3.4).  Token micro-batches arrive with top-k
+ * expert ids; the stage
+ *   1. groups their slots by local expert with a stable counting sort
+ *      (the per-expert token counts are the dispatch metadata of section
+ *      3.2.1 and Table 2),
+ *   2. runs each local expert's SwiGLU FFN as a grouped matrix
+ *      multiplication, hidden states on the left and the expert's weights on
+ *      the right (section 3.4.2, "Bubble-Free Kernel Dispatching"),
+ *   3. reduces the k expert results of each token with its routing weights
+ *      back into token order (section 3.2.2; Table 2 stores k result rows per
+ *      token), and
+ *   4. does all of it on the caller's stream per micro-batch, without any
+ *      device-wide barrier or host read-back (sections 3.4.1 and 3.4.2).
+ *
+ * Conventions (section 3.2: buffers are allocated once at initialisation and
+ * live as long as the framework; weights stay resident in HBM):
+ *   - moe_stage_create copies the weights into stage-owned device memory and
+ *     allocates every workspace buffer; no enqueue call allocates memory.
+ *   - All pointers in moe_weights / moe_microbatch are DEVICE pointers.
+ *     Micro-batch buffers are borrowed: they must stay valid and unmodified
+ *     until the work enqueued on `stream` has completed.
+ *   - `stream` is a hipStream_t passed as void*; NULL means the default stream.
+ *   - Enqueue calls are asynchronous.  Host-detectable errors are returned
+ *     synchronously and then NOTHING has been enqueued.  Expert ids outside
+ *     [-1, n_experts) are detected on the device: the slot is skipped (as if
+ *     masked) and a sticky error word is set that moe_stage_sync reports.
+ *   - Layouts are row-major.  bf16 is the IEEE-754 binary32 upper half;
+ *     fp8 is OCP E4M3FN (bias 7, max 448, no infinities).
+ *
+ * Definition of the outputs, for one micro-batch of T tokens with ids[T][k]
+ * (slot s = t*k + j) and local experts [e0, e0 + E_loc):
+ *   counts[e]      number of slots with id e, e in [0, n_experts)
+ *   offsets[i]     sum_{i' < i} counts[e0 + i'], i in [0, E_loc]
+ *   slot_of_row[r] local slots in ascending (expert id, s) order
+ *   row_of_slot[s] row of slot s in that order, -1 if s is not local
+ *   y_r            = W_down (SiLU(W_gate x_t) * (W_up x_t)), t = slot_of_row[r] / k
+ *   out[t]         = base_t + sum_{j ascending, row_of_slot[t*k+j] >= 0}
+ *                            w[t][j] * y_{row_of_slot[t*k+j]}
+ *   base_t         = 0 (MOE_COMBINE_OVERWRITE) or the previous out[t]
+ *                    (MOE_COMBINE_ACCUMULATE), plus the shared expert's
+ *                    output when the stage has one.
+ * Intermediate rows (X_perm, H, Y_perm) are stored in bf16 (fp8 mode: X_perm
+ * and H as e4m3 with per-128-channel fp32 scales); the combine accumulates in
+ * fp32 and rounds once to bf16.  Tokens with no local slot are written as
+ * +0.0 (overwrite) or left untouched (accumulate).  The combine uses no
+ * atomics, so results are bit-identical from run to run and independent of
+ * how micro-batches are spread over streams.
+ */
+#ifndef MOE_STAGE_H
+#define MOE_STAGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_API __attribute__((visibility("default")))
+
+/* Opaque stage handle, owned by the library (create / destroy). */
+typedef struct moe_stage moe_stage;
+
+typedef int32_t moe_status;
+#define MOE_OK              0
+#define MOE_EINVAL         (-1)   /* bad argument (null pointer, bad slot, size) */
+#define MOE_ENOMEM         (-2)   /* device allocation failed in create */
+#define MOE_EHIP           (-3)   /* a HIP runtime call failed */
+#define MOE_EBADID         (-4)   /* device saw an expert id outside [-1, n_experts) */
+#define MOE_EUNSUPPORTED   (-5)   /* shape or mode this build does not support */
+#define MOE_EBUSY          (-6)   /* slot still in flight (non-blocking query) */
+
+enum { MOE_DTYPE_BF16 = 0, MOE_DTYPE_FP8_E4M3_B128 = 1 };
+enum { MOE_COMBINE_OVERWRITE = 0, MOE_COMBINE_ACCUMULATE = 1 };
+
+/* Stage shape.  Requirements: d_model and d_ff multiples of 128;
+ * 1 <= n_experts <= 1024; 0 <= first_local_expert;
+ * 1 <= n_local_experts <= 256; first_local_expert + n_local_experts <=
+ * n_experts; 1 <= top_k <= 32; 0 <= max_tokens; 1 <= n_slots <= 64. */
+typedef struct {
+    int32_t d_model;             /* hidden size d (paper: H) */
+    int32_t d_ff;                /* expert intermediate size f */
+    int32_t n_experts;           /* routed experts in the model (paper: E_total) */
+    int32_t first_local_expert;  /* e0 */
+    int32_t n_local_experts;     /* E_loc */
+    int32_t top_k;               /* k */
+    int32_t max_tokens;          /* largest micro-batch (paper: S) */
+    int32_t n_slots;             /* micro-batches that may be in flight at once */
+    int32_t dtype;               /* MOE_DTYPE_* */
+    int32_t has_shared_expert;   /* 1: one always-on shared SwiGLU expert */
+} moe_stage_desc;
+
+/* Expert weights (device pointers; read during create only).
+ * bf16:  w_gate, w_up [E_loc][f][d] bf16; w_down [E_loc][d][f] bf16.
+ * fp8:   the same shapes as e4m3 bytes, with fp32 scales per 128x128 block:
+ *        s_gate, s_up [E_loc][f/128][d/128], s_down [E_loc][d/128][f/128].
+ * sh_*:  the shared expert, same layout with E_loc = 1 (NULL if none). */
+typedef struct {
+    const void  *w_gate, *w_up, *w_down;
+    const float *s_gate, *s_up, *s_down;
+    const void  *sh_gate, *sh_up, *sh_down;
+    const float *sh_s_gate, *sh_s_up, *sh_s_down;
+} moe_weights;
+
+/* One micro-batch (device pointers).
+ * x:        [T][d] bf16, or [T][d] e4m3 in fp8 mode
+ * x_scales: fp8 mode only, [T][d/128] fp32 (see moe_quantize_fp8)
+ * topk_ids: [T][k] int32, -1 = masked slot
+ * topk_w:   [T][k] fp32 routing weights
+ * out:      [T][d] bf16 */
+typedef struct {
+    int32_t        n_tokens;
+    const void    *x;
+    const float   *x_scales;
+    const int32_t *topk_ids;
+    const float   *topk_w;
+    void          *out;
+    int32_t        combine_mode;   /* MOE_COMBINE_* */
+} moe_microbatch;
+
+/* Device pointers into one slot's workspace (for tests and inspection).
+ * Valid after the slot's work has completed; overwritten by its next use. */
+typedef struct {
+    int32_t *counts;          /* [n_experts] */
+    int32_t *offsets;         /* [E_loc + 1] */
+    int32_t *slot_of_row;     /* [capacity_rows] */
+    int32_t *row_of_slot;     /* [max_tokens * k] */
+    void    *x_perm;          /* [capacity_rows][d] bf16 or e4m3 */
+    float   *x_perm_scales;   /* fp8: [capacity_rows][d/128] */
+    void    *h;               /* [capacity_rows][f] bf16 or e4m3 */
+    float   *h_scales;        /* fp8: [capacity_rows][f/128] */
+    void    *y_perm;          /* [capacity_rows][d] bf16 */
+    void    *h_shared;        /* shared expert: [max_tokens][f] */
+    float   *h_shared_scales; /* fp8 shared expert: [max_tokens][f/128] */
+    void    *y_shared;        /* shared expert: [max_tokens][d] bf16 */
+    int32_t  capacity_rows;   /* max_tokens * k */
+    int32_t  n_tokens;        /* T of the micro-batch last dispatched here */
+} moe_dispatch_view;
+
+/* Validates `desc`, copies the weights into stage-owned HBM (packed for the
+ * grouped GEMM) and allocates all workspace for n_slots micro-batches of up
+ * to max_tokens tokens.  Synchronous.  On error *out is NULL. */
+MOE_API moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *weights,
+                            moe_stage **out);
+
+/* Waits for all work of the stage and frees it.  NULL is a no-op. */
+MOE_API void moe_stage_destroy(moe_stage *stage);
+
+/* Steps 1 (histogram, scan, stable scatter, row gather) on `slot`'s
+ * workspace.  Records the micro-batch for the slot's later calls. */
+MOE_API moe_status moe_dispatch(moe_stage *stage, int32_t slot, const moe_microbatch *mb,
+                        void *stream);
+
+/* Step 2: grouped GEMM gate/up with fused SiLU*up epilogue, then grouped GEMM
+ * down, for every local expert with rows (and the shared expert, if any).
+ * The tile schedule is built on the device by moe_dispatch. */
+MOE_API moe_status moe_expert_ffn(moe_stage *stage, int32_t slot, void *stream);
+
+/* Step 3: weighted combine into mb->out (deterministic, no atomics). */
+MOE_API moe_status moe_combine(moe_stage *stage, int32_t slot, void *stream);
+
+/* Steps 1-3 on `stream` for one micro-batch, on the next slot of the
+ * stage's ring.  Never blocks the host: if that slot's previous micro-batch
+ * may still be in flight, `stream` first waits on the device for exactly that
+ * one (the backpressure of section 3.2.1, without a global barrier).
+ * *slot_out (may be NULL) receives the slot used. */
+MOE_API moe_status moe_stage_submit_microbatch(moe_stage *stage, const moe_microbatch *mb,
+                                       void *stream, int32_t *slot_out);
+
+/* Sender-side activation quantiser for the fp8 variant: per token, per 128
+ * channels, scale = amax / 448 in fp32 (1 if amax = 0), code = e4m3 of
+ * x / scale (fp32 division, round to nearest even).  x_bf16 [T][d],
+ * x_q [T][d] bytes, x_s [T][d/128] fp32.  d must be a multiple of 128. */
+MOE_API moe_status moe_quantize_fp8(const void *x_bf16, int32_t n_tokens, int32_t d_model,
+                            void *x_q, float *x_s, void *stream);
+
+/* Fills `out` with the device pointers of `slot`'s workspace. */
+MOE_API moe_status moe_stage_query(moe_stage *stage, int32_t slot, moe_dispatch_view *out);
+
+/* Waits until every slot's enqueued work has completed and returns (then
+ * clears) the sticky device error: MOE_EBADID if a kernel saw an invalid
+ * expert id since the last sync, else MOE_OK (or MOE_EHIP). */
+MOE_API moe_status moe_stage_sync(moe_stage *stage);
+
+/* Bytes of device memory moe_stage_create allocates for `desc` (weights plus
+ * workspace).  Host-only arithmetic; needs no GPU. */
+MOE_API moe_status moe_stage_workspace_bytes(const moe_stage_desc *desc, int64_t *bytes);
+
+/* Static text for a status code. */
+MOE_API const char *moe_status_string(moe_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_STAGE_H */

@@ -67,7 +67,7 @@ def dispatch(ids: np.ndarray, E: int, e0: int, E_loc: int) -> Dict[str, np.ndarr
     T, k = ids.shape
     counts = np.zeros(E, np.int32)
     offsets = np.zeros(E_loc + 1, np.int32)
-    slot_of_row = np.zeros(max(T * min(k, E_loc) if E_loc else 0, 1), np.int32)
+    slot_of_row = np.zeros(max(T * k, 1), np.int32)       # repeated ids: every slot may be local
     row_of_slot = np.zeros(max(T * k, 1), np.int32)
     n_bad = np.zeros(1, np.int32)
     n_loc = _load().oracle_dispatch(T, k, E, e0, E_loc, _i32p(ids), _i32p(counts),

@@ -1,0 +1,44 @@
+// Shared definitions of the gfx950 (CDNA4) kernels of the MoE expert stage.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+// Dispatch: slots handled by one workgroup of the histogram / scatter kernels.
+constexpr int kDispatchThreads = 256;
+constexpr int kDispatchChunk = 4096;            // 16 slots per thread
+constexpr int kMaxExperts = 1024;               // LDS histogram size
+constexpr int kMaxLocalExperts = 256;
+
+// Grouped GEMM tile: 256 x 256 output, K step 64 bf16 (or 128 e4m3) = 128 B
+// per row, four 64-wide waves each owning a 128 x 128 quadrant.
+constexpr int kBM = 256;
+constexpr int kBN = 256;
+constexpr int kGemmThreads = 256;
+
+// Sticky error bits.
+constexpr int kErrBadId = 1;
+
+// Device-side tables written by the dispatch scan, read by the GEMMs.
+struct GroupTable {
+    int32_t *row0;      // [G] first row of the group in its A matrix
+    int32_t *rows;      // [G] rows of the group
+    int32_t *mt_base;   // [G+1] prefix of ceil(rows / kBM)
+};
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Round-to-nearest-even fp32 -> bf16 (finite inputs).
+__device__ __forceinline__ bf16 f2bf(float v) { return static_cast<bf16>(v); }
+__device__ __forceinline__ float bf2f(bf16 v) { return static_cast<float>(v); }
+
+}  // namespace moe

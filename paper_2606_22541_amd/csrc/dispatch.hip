@@ -1,0 +1,206 @@
+// Dispatch of one micro-batch: per-expert histogram, scan, stable counting-sort
+// scatter and coalesced row gather.
+//
+// The per-expert token counts are the metadata the paper's MoE devices receive
+// with each batch, and the payload is grouped by expert (section 3.2.1,
+// Table 2).  Here the stage derives them itself from the top-k ids.
+//
+// The order within an expert is ascending slot index s = t*k + j.  It is
+// produced without any atomic deciding an order: each workgroup owns a
+// contiguous chunk of slots, each wave a contiguous part of the chunk, and
+// ranks inside a 64-slot step come from wave ballots, so the result is the
+// stable counting sort, bit for bit.
+#include "kernels.h"
+
+namespace moe {
+
+// ---------------------------------------------------------------------------
+// 1. Histogram over all experts, one row of counts per workgroup.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kDispatchThreads)
+void k_hist(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E,
+            int32_t *__restrict__ blk_counts, int32_t *__restrict__ err)
+{
+    __shared__ int32_t h[kMaxExperts];
+    for (int e = threadIdx.x; e < E; e += kDispatchThreads) h[e] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kDispatchChunk;
+    int bad = 0;
+    for (int i = threadIdx.x; i < kDispatchChunk; i += kDispatchThreads) {
+        int64_t s = base + i;
+        if (s >= n_slots) break;
+        int e = ids[s];
+        if (e >= 0 && e < E) atomicAdd(&h[e], 1);       // integer counts: order-free
+        else if (e != -1) bad = 1;
+    }
+    if (bad) atomicOr(err, kErrBadId);
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += kDispatchThreads)
+        blk_counts[(int64_t)blockIdx.x * E + e] = h[e];
+}
+
+// ---------------------------------------------------------------------------
+// 2. Scan (single workgroup): global counts, local offsets, per-workgroup
+//    bases, and the grouped-GEMM tile table.  Nothing returns to the host.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(1024)
+void k_scan(const int32_t *__restrict__ blk_counts, int32_t nb, int32_t E, int32_t e0,
+            int32_t E_loc, int32_t T, int32_t has_shared, int32_t *__restrict__ counts,
+            int32_t *__restrict__ offsets, int32_t *__restrict__ blk_base, GroupTable g)
+{
+    __shared__ int32_t c[kMaxExperts];
+    __shared__ int32_t off[kMaxLocalExperts + 1];
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        int acc = 0;
+        for (int b = 0; b < nb; ++b) acc += blk_counts[(int64_t)b * E + e];
+        c[e] = acc;
+        counts[e] = acc;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int i = 0; i < E_loc; ++i) { off[i] = run; run += c[e0 + i]; }
+        off[E_loc] = run;
+        // tile table over G = E_loc (+1 shared) groups
+        int mt = 0;
+        for (int i = 0; i < E_loc; ++i) {
+            g.row0[i] = off[i];
+            g.rows[i] = c[e0 + i];
+            g.mt_base[i] = mt;
+            mt += (c[e0 + i] + kBM - 1) / kBM;
+        }
+        if (has_shared) {
+            g.row0[E_loc] = 0;
+            g.rows[E_loc] = T;
+            g.mt_base[E_loc] = mt;
+            mt += (T + kBM - 1) / kBM;
+        }
+        g.mt_base[E_loc + (has_shared ? 1 : 0)] = mt;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i <= E_loc; i += blockDim.x) offsets[i] = off[i];
+    for (int i = threadIdx.x; i < E_loc; i += blockDim.x) {
+        int run = off[i];
+        for (int b = 0; b < nb; ++b) {
+            blk_base[(int64_t)b * E_loc + i] = run;
+            run += blk_counts[(int64_t)b * E + e0 + i];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 3. Stable scatter.  Wave w of workgroup b owns slots
+//    [b*chunk + w*chunk/4, b*chunk + (w+1)*chunk/4) and walks them in 64-slot
+//    steps; within a step, lanes holding the same expert are ranked by lane
+//    order with a ballot.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kDispatchThreads)
+void k_scatter(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E, int32_t e0,
+               int32_t E_loc, const int32_t *__restrict__ blk_base,
+               int32_t *__restrict__ slot_of_row, int32_t *__restrict__ row_of_slot)
+{
+    constexpr int kWaves = kDispatchThreads / 64;
+    constexpr int kPerWave = kDispatchChunk / kWaves;
+    __shared__ int32_t wbase[kWaves][kMaxLocalExperts];
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int64_t wstart = (int64_t)blockIdx.x * kDispatchChunk + (int64_t)wave * kPerWave;
+
+    for (int i = lane; i < E_loc; i += 64) wbase[wave][i] = 0;
+    __syncthreads();
+    // per-wave local counts
+    for (int st = 0; st < kPerWave; st += 64) {
+        int64_t s = wstart + st + lane;
+        int e = (s < n_slots) ? ids[s] : -1;
+        int i = e - e0;
+        if (e >= 0 && e < E && i >= 0 && i < E_loc) atomicAdd(&wbase[wave][i], 1);
+    }
+    __syncthreads();
+    // exclusive scan over waves, seeded with this workgroup's base
+    for (int i = threadIdx.x; i < E_loc; i += kDispatchThreads) {
+        int run = blk_base[(int64_t)blockIdx.x * E_loc + i];
+        for (int w = 0; w < kWaves; ++w) {
+            int t = wbase[w][i];
+            wbase[w][i] = run;
+            run += t;
+        }
+    }
+    __syncthreads();
+    volatile int32_t *mybase = wbase[wave];
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int st = 0; st < kPerWave; st += 64) {
+        int64_t s = wstart + st + lane;
+        bool in = s < n_slots;
+        int e = in ? ids[s] : -1;
+        int i = e - e0;
+        bool loc = in && e >= 0 && e < E && i >= 0 && i < E_loc;
+        uint64_t pending = __ballot(loc);
+        int pos = -1;
+        while (pending) {
+            int leader = __ffsll((unsigned long long)pending) - 1;
+            int il = __shfl(i, leader);
+            uint64_t m = __ballot(loc && i == il);
+            int b = mybase[il];
+            if (loc && i == il) pos = b + __popcll(m & lt_mask);
+            if (lane == leader) mybase[il] = b + __popcll(m);
+            pending &= ~m;
+        }
+        if (in) {
+            row_of_slot[s] = pos;
+            if (pos >= 0) slot_of_row[pos] = (int32_t)s;
+        }
+    }
+}
+
+hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)
+{
+    const int nb = (a.n_slots + kDispatchChunk - 1) / kDispatchChunk;
+    if (nb > 0) {
+        hipLaunchKernelGGL(k_hist, dim3(nb), dim3(kDispatchThreads), 0, s, a.ids, a.n_slots, a.E,
+                           a.blk_counts, a.err);
+    }
+    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, a.blk_counts, nb, a.E, a.e0, a.E_loc,
+                       a.T, a.has_shared, a.counts, a.offsets, a.blk_base, a.groups);
+    if (nb > 0) {
+        hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(kDispatchThreads), 0, s, a.ids, a.n_slots,
+                           a.E, a.e0, a.E_loc, a.blk_base, a.slot_of_row, a.row_of_slot);
+    }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// 4. Row gather: one row per workgroup iteration, 16-byte vector copies.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256)
+void k_gather(const uint4 *__restrict__ x, const float *__restrict__ xs,
+              const int32_t *__restrict__ slot_of_row, const int32_t *__restrict__ n_rows_dev,
+              int32_t k, int32_t row_vecs, int32_t n_scales, uint4 *__restrict__ xp,
+              float *__restrict__ xps)
+{
+    const int n_rows = *n_rows_dev;
+    for (int r = blockIdx.x; r < n_rows; r += gridDim.x) {
+        const int t = slot_of_row[r] / k;
+        const uint4 *src = x + (int64_t)t * row_vecs;
+        uint4 *dst = xp + (int64_t)r * row_vecs;
+        for (int c = threadIdx.x; c < row_vecs; c += 256) dst[c] = src[c];
+        if (xs != nullptr)
+            for (int c = threadIdx.x; c < n_scales; c += 256)
+                xps[(int64_t)r * n_scales + c] = xs[(int64_t)t * n_scales + c];
+    }
+}
+
+hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_t *slot_of_row,
+                              const int32_t *n_rows_dev, int32_t k, int32_t row_bytes,
+                              int32_t n_scales, void *x_perm, float *x_perm_scales,
+                              int32_t max_rows, int num_cus, hipStream_t s)
+{
+    if (max_rows <= 0) return hipSuccess;
+    int grid = num_cus * 8;
+    if (grid > max_rows) grid = max_rows;
+    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), 0, s, (const uint4 *)x, x_scales,
+                       slot_of_row, n_rows_dev, k, row_bytes / 16, n_scales, (uint4 *)x_perm,
+                       x_perm_scales);
+    return hipGetLastError();
+}
+
+}  // namespace moe

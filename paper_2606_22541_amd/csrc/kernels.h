@@ -1,0 +1,89 @@
+// Host-side launchers of the stage's kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace moe {
+
+struct DispatchArgs {
+    const int32_t *ids;      // [T*k]
+    int32_t n_slots;         // T*k
+    int32_t T, k, E, e0, E_loc;
+    int32_t has_shared;
+    int32_t *blk_counts;     // [nb][E]
+    int32_t *counts;         // [E]
+    int32_t *offsets;        // [E_loc+1]
+    int32_t *blk_base;       // [nb][E_loc]
+    GroupTable groups;       // G = E_loc + has_shared groups
+    int32_t *slot_of_row;    // [cap]
+    int32_t *row_of_slot;    // [T*k]
+    int32_t *err;            // sticky error word
+};
+
+// Histogram -> scan (+ GEMM tile table) -> stable scatter.
+hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s);
+
+// X_perm[r] = x[slot_of_row[r] / k] for r < offsets[E_loc].  row_bytes is the
+// byte length of one activation row (2d for bf16, d for e4m3); when
+// scales != nullptr the per-row fp32 scales (n_scales per row) move as well.
+hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_t *slot_of_row,
+                              const int32_t *n_rows_dev, int32_t k, int32_t row_bytes,
+                              int32_t n_scales, void *x_perm, float *x_perm_scales,
+                              int32_t max_rows, int num_cus, hipStream_t s);
+
+struct GemmArgs {
+    const void *A_routed;    // [rows][K] (rows of X_perm or H)
+    const void *A_shared;    // [T][K] (x or H_shared) for group E_loc, if shared
+    const float *As_routed;  // fp8: [rows][K/128] scales of A
+    const float *As_shared;
+    const void *B;           // [G][N][K] weights (K contiguous)
+    const float *Bs;         // fp8: block scales
+    void *C_routed;          // [rows][ldc]
+    void *C_shared;
+    float *Cs_routed;        // fp8 SwiGLU epilogue: [rows][f/128] scales of H
+    float *Cs_shared;
+    int32_t N, K;
+    int32_t shared_group;    // index of the shared group, -1 if none
+    GroupTable groups;
+    int32_t G;
+};
+
+// bf16 grouped GEMM.  swiglu = true: B is the packed [gate|up] matrix
+// (N = 2f) and C receives SiLU(gate) * up as [rows][f] bf16; otherwise C
+// receives the product as [rows][N] bf16.
+hipError_t launch_gemm_bf16(const GemmArgs &a, bool swiglu, int max_tiles, int num_cus,
+                            hipStream_t s);
+
+// e4m3 grouped GEMM with 128-block scales (same conventions; the SwiGLU
+// epilogue also quantises h per 128 channels).
+hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int max_tiles, int num_cus,
+                           hipStream_t s);
+
+struct CombineArgs {
+    const void *y_perm;        // [rows][d] bf16
+    const void *y_shared;      // [T][d] bf16 or nullptr
+    const int32_t *row_of_slot;
+    const float *w;            // [T][k]
+    void *out;                 // [T][d] bf16
+    int32_t T, k, d, accumulate;
+};
+hipError_t launch_combine(const CombineArgs &a, int num_cus, hipStream_t s);
+
+hipError_t launch_quantize_fp8(const void *x, int32_t T, int32_t d, void *xq, float *xs,
+                               int num_cus, hipStream_t s);
+
+// Weight packing at create time.
+// Interleaves gate and up rows in blocks of 32: packed row 64*b + i is gate
+// row 32*b + i for i < 32 and up row 32*b + (i - 32) otherwise.  elem_bytes
+// is 2 (bf16) or 1 (e4m3).
+hipError_t launch_pack_gate_up(const void *gate, const void *up, void *packed, int32_t n_mats,
+                               int32_t f, int32_t d, int32_t elem_bytes, hipStream_t s);
+// Per-32-row scales of the packed matrix from the 128x128 block scales:
+// packed_s[m][p32][kb] = (gate or up)_s[m][(32*b)/128][kb].
+hipError_t launch_pack_gate_up_scales(const float *gs, const float *us, float *packed_s,
+                                      int32_t n_mats, int32_t f, int32_t d, hipStream_t s);
+
+}  // namespace moe

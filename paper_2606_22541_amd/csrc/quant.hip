@@ -1,0 +1,118 @@
+// fp8 helpers: the sender-side activation quantiser and the create-time
+// weight packing kernels.
+#include "kernels.h"
+
+namespace moe {
+
+// e4m3 (OCP E4M3FN) code of v, round to nearest even.  |v| is clamped to 448
+// first, which makes the conversion saturating.
+__device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float d)
+{
+    a = fminf(fmaxf(a, -448.0f), 448.0f);
+    b = fminf(fmaxf(b, -448.0f), 448.0f);
+    c = fminf(fmaxf(c, -448.0f), 448.0f);
+    d = fminf(fmaxf(d, -448.0f), 448.0f);
+    int v = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+    v = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, v, true);
+    return (uint32_t)v;
+}
+
+// One group of 128 channels is handled by 16 lanes, 8 channels each.
+__global__ __launch_bounds__(256)
+void k_quantize_fp8(const uint4 *__restrict__ x, int32_t T, int32_t groups_per_row,
+                    uint2 *__restrict__ xq, float *__restrict__ xs)
+{
+    const int64_t n_groups = (int64_t)T * groups_per_row;
+    const int sub = threadIdx.x & 15;
+    for (int64_t gi = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 4; gi < n_groups;
+         gi += ((int64_t)gridDim.x * 256) >> 4) {
+        uint4 v = x[gi * 16 + sub];
+        const bf16 *vb = (const bf16 *)&v;
+        float f[8];
+        float amax = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            f[i] = bf2f(vb[i]);
+            amax = fmaxf(amax, fabsf(f[i]));
+        }
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) amax = fmaxf(amax, __shfl_xor(amax, m, 16));
+        const float s = amax > 0.0f ? amax / 448.0f : 1.0f;   // IEEE division
+        uint2 q;
+        q.x = e4m3_pack4(f[0] / s, f[1] / s, f[2] / s, f[3] / s);
+        q.y = e4m3_pack4(f[4] / s, f[5] / s, f[6] / s, f[7] / s);
+        xq[gi * 16 + sub] = q;
+        if (sub == 0) xs[gi] = s;
+    }
+}
+
+hipError_t launch_quantize_fp8(const void *x, int32_t T, int32_t d, void *xq, float *xs,
+                               int num_cus, hipStream_t s)
+{
+    if (T <= 0) return hipSuccess;
+    const int gpr = d / 128;
+    const int64_t threads = (int64_t)T * gpr * 16;
+    int64_t grid = (threads + 255) / 256;
+    if (grid > (int64_t)num_cus * 16) grid = (int64_t)num_cus * 16;
+    hipLaunchKernelGGL(k_quantize_fp8, dim3((unsigned)grid), dim3(256), 0, s, (const uint4 *)x,
+                       T, gpr, (uint2 *)xq, xs);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Weight packing (create time only).
+// ---------------------------------------------------------------------------
+__global__ void k_pack_gate_up(const uint4 *__restrict__ gate, const uint4 *__restrict__ up,
+                               uint4 *__restrict__ packed, int32_t n_mats, int32_t f,
+                               int32_t row_vecs)
+{
+    const int64_t total = (int64_t)n_mats * 2 * f * row_vecs;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t prow = q / row_vecs;
+        const int c = (int)(q - prow * row_vecs);
+        const int m = (int)(prow / (2 * f));
+        const int p = (int)(prow - (int64_t)m * 2 * f);
+        const int b = p >> 6, i = p & 63;
+        const int src_row = b * 32 + (i & 31);
+        const uint4 *src = (i < 32) ? gate : up;
+        packed[q] = src[((int64_t)m * f + src_row) * row_vecs + c];
+    }
+}
+
+hipError_t launch_pack_gate_up(const void *gate, const void *up, void *packed, int32_t n_mats,
+                               int32_t f, int32_t d, int32_t elem_bytes, hipStream_t s)
+{
+    const int row_vecs = d * elem_bytes / 16;
+    hipLaunchKernelGGL(k_pack_gate_up, dim3(4096), dim3(256), 0, s, (const uint4 *)gate,
+                       (const uint4 *)up, (uint4 *)packed, n_mats, f, row_vecs);
+    return hipGetLastError();
+}
+
+__global__ void k_pack_gate_up_scales(const float *__restrict__ gs, const float *__restrict__ us,
+                                      float *__restrict__ ps, int32_t n_mats, int32_t f,
+                                      int32_t kblocks)
+{
+    const int p32n = 2 * f / 32;
+    const int64_t total = (int64_t)n_mats * p32n * kblocks;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int kb = (int)(q % kblocks);
+        const int64_t rest = q / kblocks;
+        const int p32 = (int)(rest % p32n);
+        const int m = (int)(rest / p32n);
+        const int fblk = ((p32 >> 1) * 32) / 128;
+        const float *src = (p32 & 1) ? us : gs;
+        ps[q] = src[((int64_t)m * (f / 128) + fblk) * kblocks + kb];
+    }
+}
+
+hipError_t launch_pack_gate_up_scales(const float *gs, const float *us, float *packed_s,
+                                      int32_t n_mats, int32_t f, int32_t d, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_pack_gate_up_scales, dim3(256), dim3(256), 0, s, gs, us, packed_s,
+                       n_mats, f, d / 128);
+    return hipGetLastError();
+}
+
+}  // namespace moe

@@ -1,0 +1,500 @@
+// Host runtime of the MoE expert stage: the C ABI declared in moe_stage.h.
+//
+// Everything the hot path needs is allocated in moe_stage_create (weights
+// packed for the grouped GEMM, and one workspace per in-flight micro-batch
+// slot), following the paper's statically allocated, process-lifetime
+// buffers (section 3.2).  The enqueue calls only validate arguments and
+// launch kernels on the caller's stream; per-expert row counts stay on the
+// device (section 3.4.2: host round trips are the bubble to avoid).
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "kernels.h"
+#include "moe_stage.h"
+
+using namespace moe;
+
+namespace {
+
+struct SlotWs {
+    int32_t *blk_counts = nullptr, *counts = nullptr, *offsets = nullptr, *blk_base = nullptr;
+    int32_t *g_row0 = nullptr, *g_rows = nullptr, *g_mt_base = nullptr;
+    int32_t *slot_of_row = nullptr, *row_of_slot = nullptr;
+    void *x_perm = nullptr;
+    float *x_perm_s = nullptr;
+    void *h = nullptr;
+    float *h_s = nullptr;
+    void *y_perm = nullptr;
+    void *h_sh = nullptr;
+    float *h_sh_s = nullptr;
+    void *y_sh = nullptr;
+    hipEvent_t ev = nullptr;
+    bool ev_recorded = false;
+    bool has_mb = false;
+    moe_microbatch mb{};
+};
+
+struct Sizes {
+    int64_t G, cap, nb_max, eb, n_slots_tok;
+    int64_t w1, w2, s1, s2;                 // bytes
+    int64_t per_slot;                       // bytes
+};
+
+bool desc_ok(const moe_stage_desc *d)
+{
+    if (!d) return false;
+    if (d->d_model <= 0 || d->d_model % 128 || d->d_ff <= 0 || d->d_ff % 128) return false;
+    if (d->n_experts < 1 || d->n_experts > kMaxExperts) return false;
+    if (d->first_local_expert < 0 || d->n_local_experts < 1 ||
+        d->n_local_experts > kMaxLocalExperts ||
+        d->first_local_expert + d->n_local_experts > d->n_experts)
+        return false;
+    if (d->top_k < 1 || d->top_k > 32) return false;
+    if (d->max_tokens < 0 || d->n_slots < 1 || d->n_slots > 64) return false;
+    if (d->dtype != MOE_DTYPE_BF16 && d->dtype != MOE_DTYPE_FP8_E4M3_B128) return false;
+    if (d->has_shared_expert != 0 && d->has_shared_expert != 1) return false;
+    // 32-bit slot and row indices; 32-bit byte offsets inside one GEMM tile
+    if ((int64_t)d->max_tokens * d->top_k >= (int64_t)1 << 31) return false;
+    if ((int64_t)256 * d->d_model * 2 >= (int64_t)1 << 31) return false;
+    if ((int64_t)256 * d->d_ff * 2 >= (int64_t)1 << 31) return false;
+    return true;
+}
+
+int64_t align256(int64_t b) { return (b + 255) & ~(int64_t)255; }
+
+Sizes sizes_of(const moe_stage_desc *d)
+{
+    Sizes s{};
+    const int64_t D = d->d_model, F = d->d_ff, E = d->n_experts, El = d->n_local_experts;
+    const int64_t k = d->top_k, T = d->max_tokens;
+    const bool fp8 = d->dtype == MOE_DTYPE_FP8_E4M3_B128;
+    s.G = El + d->has_shared_expert;
+    s.eb = fp8 ? 1 : 2;
+    s.cap = T * k;   // a token may repeat a local id, so every slot can be local
+    s.n_slots_tok = T * k;
+    s.nb_max = (s.n_slots_tok + kDispatchChunk - 1) / kDispatchChunk;
+    if (s.nb_max < 1) s.nb_max = 1;
+    s.w1 = align256(s.G * 2 * F * D * s.eb);
+    s.w2 = align256(s.G * D * F * s.eb);
+    s.s1 = fp8 ? align256(s.G * (2 * F / 32) * (D / 128) * 4) : 0;
+    s.s2 = fp8 ? align256(s.G * (D / 128) * (F / 128) * 4) : 0;
+    const int64_t cap1 = s.cap > 0 ? s.cap : 1;
+    const int64_t T1 = T > 0 ? T : 1;
+    int64_t b = 0;
+    b += align256(s.nb_max * E * 4) + align256(E * 4) + align256((El + 1) * 4);
+    b += align256(s.nb_max * El * 4);
+    b += 2 * align256(s.G * 4) + align256((s.G + 1) * 4);
+    b += align256(cap1 * 4) + align256((s.n_slots_tok > 0 ? s.n_slots_tok : 1) * 4);
+    b += align256(cap1 * D * s.eb) + (fp8 ? align256(cap1 * (D / 128) * 4) : 0);
+    b += align256(cap1 * F * s.eb) + (fp8 ? align256(cap1 * (F / 128) * 4) : 0);
+    b += align256(cap1 * D * 2);
+    if (d->has_shared_expert) {
+        b += align256(T1 * F * s.eb) + (fp8 ? align256(T1 * (F / 128) * 4) : 0);
+        b += align256(T1 * D * 2);
+    }
+    s.per_slot = b;
+    return s;
+}
+
+}  // namespace
+
+struct moe_stage {
+    moe_stage_desc desc{};
+    Sizes sz{};
+    int device = 0;
+    int num_cus = 0;
+    void *w1 = nullptr, *w2 = nullptr;
+    float *s1 = nullptr, *s2 = nullptr;
+    int32_t *err = nullptr;
+    hipStream_t own = nullptr;
+    std::vector<SlotWs> slots;
+    std::vector<void *> allocs;
+    int next_slot = 0;
+};
+
+namespace {
+
+void release(moe_stage *st)
+{
+    if (!st) return;
+    for (auto &sl : st->slots) {
+        if (sl.ev) {
+            hipEventSynchronize(sl.ev);
+            hipEventDestroy(sl.ev);
+        }
+    }
+    if (st->own) {
+        hipStreamSynchronize(st->own);
+        hipStreamDestroy(st->own);
+    }
+    for (void *p : st->allocs) hipFree(p);
+    delete st;
+}
+
+template <typename T>
+bool alloc(moe_stage *st, T **p, int64_t bytes)
+{
+    void *q = nullptr;
+    if (hipMalloc(&q, (size_t)align256(bytes > 0 ? bytes : 4)) != hipSuccess) return false;
+    st->allocs.push_back(q);
+    *p = (T *)q;
+    return true;
+}
+
+bool slot_ok(const moe_stage *st, int32_t slot)
+{
+    return st && slot >= 0 && slot < (int32_t)st->slots.size();
+}
+
+moe_status record(SlotWs &sl, hipStream_t s)
+{
+    if (hipEventRecord(sl.ev, s) != hipSuccess) return MOE_EHIP;
+    sl.ev_recorded = true;
+    return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *moe_status_string(moe_status s)
+{
+    switch (s) {
+    case MOE_OK: return "ok";
+    case MOE_EINVAL: return "invalid argument";
+    case MOE_ENOMEM: return "out of device memory";
+    case MOE_EHIP: return "HIP runtime error";
+    case MOE_EBADID: return "expert id outside [-1, n_experts) seen on the device";
+    case MOE_EUNSUPPORTED: return "unsupported shape or mode";
+    case MOE_EBUSY: return "slot busy";
+    default: return "unknown status";
+    }
+}
+
+moe_status moe_stage_workspace_bytes(const moe_stage_desc *desc, int64_t *bytes)
+{
+    if (!bytes) return MOE_EINVAL;
+    if (!desc_ok(desc)) return MOE_EINVAL;
+    Sizes s = sizes_of(desc);
+    *bytes = s.w1 + s.w2 + s.s1 + s.s2 + 256 + s.per_slot * desc->n_slots;
+    return MOE_OK;
+}
+
+moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, moe_stage **out)
+{
+    if (!out) return MOE_EINVAL;
+    *out = nullptr;
+    if (!desc_ok(desc) || !w) return MOE_EINVAL;
+    const bool fp8 = desc->dtype == MOE_DTYPE_FP8_E4M3_B128;
+    if (!w->w_gate || !w->w_up || !w->w_down) return MOE_EINVAL;
+    if (fp8 && (!w->s_gate || !w->s_up || !w->s_down)) return MOE_EINVAL;
+    if (desc->has_shared_expert) {
+        if (!w->sh_gate || !w->sh_up || !w->sh_down) return MOE_EINVAL;
+        if (fp8 && (!w->sh_s_gate || !w->sh_s_up || !w->sh_s_down)) return MOE_EINVAL;
+    }
+
+    moe_stage *st = new (std::nothrow) moe_stage();
+    if (!st) return MOE_ENOMEM;
+    st->desc = *desc;
+    st->sz = sizes_of(desc);
+    const Sizes &z = st->sz;
+    if (hipGetDevice(&st->device) != hipSuccess ||
+        hipDeviceGetAttribute(&st->num_cus, hipDeviceAttributeMultiprocessorCount, st->device) !=
+            hipSuccess ||
+        hipStreamCreateWithFlags(&st->own, hipStreamNonBlocking) != hipSuccess) {
+        release(st);
+        return MOE_EHIP;
+    }
+    const int64_t D = desc->d_model, F = desc->d_ff, El = desc->n_local_experts;
+    bool ok = alloc(st, &st->w1, z.w1) && alloc(st, &st->w2, z.w2) && alloc(st, &st->err, 4);
+    if (ok && fp8) ok = alloc(st, &st->s1, z.s1) && alloc(st, &st->s2, z.s2);
+    if (!ok) {
+        release(st);
+        return MOE_ENOMEM;
+    }
+    // Pack the weights: [gate|up] interleaved by 32 rows, down as is; the
+    // shared expert is group E_loc.
+    hipError_t e = hipSuccess;
+    const int64_t w1_mat = 2 * F * D * z.eb, w2_mat = D * F * z.eb;
+    e = launch_pack_gate_up(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)F, (int32_t)D,
+                            (int32_t)z.eb, st->own);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(st->w2, w->w_down, (size_t)(El * w2_mat), hipMemcpyDeviceToDevice,
+                           st->own);
+    if (e == hipSuccess && desc->has_shared_expert) {
+        e = launch_pack_gate_up(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
+                                (int32_t)F, (int32_t)D, (int32_t)z.eb, st->own);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync((char *)st->w2 + El * w2_mat, w->sh_down, (size_t)w2_mat,
+                               hipMemcpyDeviceToDevice, st->own);
+    }
+    if (e == hipSuccess && fp8) {
+        const int64_t s1_mat = (2 * F / 32) * (D / 128), s2_mat = (D / 128) * (F / 128);
+        e = launch_pack_gate_up_scales(w->s_gate, w->s_up, st->s1, (int32_t)El, (int32_t)F,
+                                       (int32_t)D, st->own);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(st->s2, w->s_down, (size_t)(El * s2_mat * 4),
+                               hipMemcpyDeviceToDevice, st->own);
+        if (e == hipSuccess && desc->has_shared_expert) {
+            e = launch_pack_gate_up_scales(w->sh_s_gate, w->sh_s_up, st->s1 + El * s1_mat, 1,
+                                           (int32_t)F, (int32_t)D, st->own);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(st->s2 + El * s2_mat, w->sh_s_down, (size_t)(s2_mat * 4),
+                                   hipMemcpyDeviceToDevice, st->own);
+        }
+    }
+    if (e == hipSuccess) e = hipMemsetAsync(st->err, 0, 4, st->own);
+    if (e != hipSuccess) {
+        release(st);
+        return MOE_EHIP;
+    }
+
+    st->slots.resize(desc->n_slots);
+    const int64_t E = desc->n_experts, cap1 = z.cap > 0 ? z.cap : 1;
+    const int64_t T1 = desc->max_tokens > 0 ? desc->max_tokens : 1;
+    for (auto &sl : st->slots) {
+        ok = alloc(st, &sl.blk_counts, z.nb_max * E * 4) && alloc(st, &sl.counts, E * 4) &&
+             alloc(st, &sl.offsets, (El + 1) * 4) && alloc(st, &sl.blk_base, z.nb_max * El * 4) &&
+             alloc(st, &sl.g_row0, z.G * 4) && alloc(st, &sl.g_rows, z.G * 4) &&
+             alloc(st, &sl.g_mt_base, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
+             alloc(st, &sl.row_of_slot, (z.n_slots_tok > 0 ? z.n_slots_tok : 1) * 4) &&
+             alloc(st, &sl.x_perm, cap1 * D * z.eb) && alloc(st, &sl.h, cap1 * F * z.eb) &&
+             alloc(st, &sl.y_perm, cap1 * D * 2);
+        if (ok && fp8) ok = alloc(st, &sl.x_perm_s, cap1 * (D / 128) * 4) &&
+                            alloc(st, &sl.h_s, cap1 * (F / 128) * 4);
+        if (ok && desc->has_shared_expert) {
+            ok = alloc(st, &sl.h_sh, T1 * F * z.eb) && alloc(st, &sl.y_sh, T1 * D * 2);
+            if (ok && fp8) ok = alloc(st, &sl.h_sh_s, T1 * (F / 128) * 4);
+        }
+        if (!ok) {
+            release(st);
+            return MOE_ENOMEM;
+        }
+        if (hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming) != hipSuccess) {
+            release(st);
+            return MOE_EHIP;
+        }
+    }
+    if (hipStreamSynchronize(st->own) != hipSuccess) {
+        release(st);
+        return MOE_EHIP;
+    }
+    *out = st;
+    return MOE_OK;
+}
+
+void moe_stage_destroy(moe_stage *st) { release(st); }
+
+static bool mb_ok(const moe_stage *st, const moe_microbatch *mb)
+{
+    if (!st || !mb) return false;
+    const moe_stage_desc &d = st->desc;
+    const int32_t T = mb->n_tokens;
+    if (T < 0 || T > d.max_tokens) return false;
+    if (mb->combine_mode != MOE_COMBINE_OVERWRITE && mb->combine_mode != MOE_COMBINE_ACCUMULATE)
+        return false;
+    if (T > 0 && (!mb->x || !mb->topk_ids || !mb->topk_w || !mb->out)) return false;
+    if (T > 0 && d.dtype == MOE_DTYPE_FP8_E4M3_B128 && !mb->x_scales) return false;
+    return true;
+}
+
+moe_status moe_dispatch(moe_stage *st, int32_t slot, const moe_microbatch *mb, void *stream)
+{
+    if (!slot_ok(st, slot) || !mb_ok(st, mb)) return MOE_EINVAL;
+    const moe_stage_desc &d = st->desc;
+    const int32_t T = mb->n_tokens;
+    const bool fp8 = d.dtype == MOE_DTYPE_FP8_E4M3_B128;
+    hipStream_t s = (hipStream_t)stream;
+    SlotWs &sl = st->slots[slot];
+    sl.mb = *mb;
+    sl.has_mb = true;
+
+    DispatchArgs a{};
+    a.ids = mb->topk_ids;
+    a.n_slots = T * d.top_k;
+    a.T = T;
+    a.k = d.top_k;
+    a.E = d.n_experts;
+    a.e0 = d.first_local_expert;
+    a.E_loc = d.n_local_experts;
+    a.has_shared = d.has_shared_expert;
+    a.blk_counts = sl.blk_counts;
+    a.counts = sl.counts;
+    a.offsets = sl.offsets;
+    a.blk_base = sl.blk_base;
+    a.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base};
+    a.slot_of_row = sl.slot_of_row;
+    a.row_of_slot = sl.row_of_slot;
+    a.err = st->err;
+    if (launch_dispatch_index(a, s) != hipSuccess) return MOE_EHIP;
+    const int64_t max_rows = (int64_t)T * d.top_k;
+    if (max_rows > 0) {
+        const int32_t row_bytes = fp8 ? d.d_model : 2 * d.d_model;
+        if (launch_gather_rows(mb->x, fp8 ? mb->x_scales : nullptr, sl.slot_of_row,
+                               sl.offsets + d.n_local_experts, d.top_k, row_bytes,
+                               d.d_model / 128, sl.x_perm, sl.x_perm_s, (int32_t)max_rows,
+                               st->num_cus, s) != hipSuccess)
+            return MOE_EHIP;
+    }
+    return record(sl, s);
+}
+
+moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
+{
+    if (!slot_ok(st, slot)) return MOE_EINVAL;
+    SlotWs &sl = st->slots[slot];
+    if (!sl.has_mb) return MOE_EINVAL;
+    const moe_stage_desc &d = st->desc;
+    const int32_t T = sl.mb.n_tokens;
+    hipStream_t s = (hipStream_t)stream;
+    if (T == 0) return record(sl, s);
+    const bool fp8 = d.dtype == MOE_DTYPE_FP8_E4M3_B128;
+    const int64_t max_rows = (int64_t)T * d.top_k;
+    int64_t mt_max = (max_rows + kBM - 1) / kBM + d.n_local_experts;
+    if (d.has_shared_expert) mt_max += (T + kBM - 1) / kBM;
+
+    GemmArgs g1{};
+    g1.A_routed = sl.x_perm;
+    g1.A_shared = sl.mb.x;
+    g1.As_routed = sl.x_perm_s;
+    g1.As_shared = sl.mb.x_scales;
+    g1.B = st->w1;
+    g1.Bs = st->s1;
+    g1.C_routed = sl.h;
+    g1.C_shared = sl.h_sh;
+    g1.Cs_routed = sl.h_s;
+    g1.Cs_shared = sl.h_sh_s;
+    g1.N = 2 * d.d_ff;
+    g1.K = d.d_model;
+    g1.shared_group = d.has_shared_expert ? d.n_local_experts : -1;
+    g1.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base};
+    g1.G = (int32_t)st->sz.G;
+
+    GemmArgs g2 = g1;
+    g2.A_routed = sl.h;
+    g2.A_shared = sl.h_sh;
+    g2.As_routed = sl.h_s;
+    g2.As_shared = sl.h_sh_s;
+    g2.B = st->w2;
+    g2.Bs = st->s2;
+    g2.C_routed = sl.y_perm;
+    g2.C_shared = sl.y_sh;
+    g2.Cs_routed = nullptr;
+    g2.Cs_shared = nullptr;
+    g2.N = d.d_model;
+    g2.K = d.d_ff;
+
+    const int64_t t1 = mt_max * ((g1.N + kBN - 1) / kBN);
+    const int64_t t2 = mt_max * ((g2.N + kBN - 1) / kBN);
+    const int mt1 = t1 > 0x7fffffff ? 0x7fffffff : (int)t1;
+    const int mt2 = t2 > 0x7fffffff ? 0x7fffffff : (int)t2;
+    hipError_t e;
+    if (fp8) {
+        e = launch_gemm_fp8(g1, true, mt1, st->num_cus, s);
+        if (e == hipSuccess) e = launch_gemm_fp8(g2, false, mt2, st->num_cus, s);
+    } else {
+        e = launch_gemm_bf16(g1, true, mt1, st->num_cus, s);
+        if (e == hipSuccess) e = launch_gemm_bf16(g2, false, mt2, st->num_cus, s);
+    }
+    if (e == hipErrorNotSupported) return MOE_EUNSUPPORTED;
+    if (e != hipSuccess) return MOE_EHIP;
+    return record(sl, s);
+}
+
+moe_status moe_combine(moe_stage *st, int32_t slot, void *stream)
+{
+    if (!slot_ok(st, slot)) return MOE_EINVAL;
+    SlotWs &sl = st->slots[slot];
+    if (!sl.has_mb) return MOE_EINVAL;
+    const moe_stage_desc &d = st->desc;
+    hipStream_t s = (hipStream_t)stream;
+    CombineArgs c{};
+    c.y_perm = sl.y_perm;
+    c.y_shared = d.has_shared_expert ? sl.y_sh : nullptr;
+    c.row_of_slot = sl.row_of_slot;
+    c.w = sl.mb.topk_w;
+    c.out = sl.mb.out;
+    c.T = sl.mb.n_tokens;
+    c.k = d.top_k;
+    c.d = d.d_model;
+    c.accumulate = sl.mb.combine_mode == MOE_COMBINE_ACCUMULATE;
+    if (launch_combine(c, st->num_cus, s) != hipSuccess) return MOE_EHIP;
+    return record(sl, s);
+}
+
+moe_status moe_stage_submit_microbatch(moe_stage *st, const moe_microbatch *mb, void *stream,
+                                       int32_t *slot_out)
+{
+    if (!mb_ok(st, mb)) return MOE_EINVAL;
+    const int32_t slot = st->next_slot;
+    SlotWs &sl = st->slots[slot];
+    hipStream_t s = (hipStream_t)stream;
+    // Backpressure: the slot's previous micro-batch must be done before its
+    // workspace is reused.  The wait is on the device, for that one event.
+    if (sl.ev_recorded && hipStreamWaitEvent(s, sl.ev, 0) != hipSuccess) return MOE_EHIP;
+    moe_status r = moe_dispatch(st, slot, mb, stream);
+    if (r != MOE_OK) return r;
+    st->next_slot = (slot + 1) % (int32_t)st->slots.size();
+    if ((r = moe_expert_ffn(st, slot, stream)) != MOE_OK) return r;
+    if ((r = moe_combine(st, slot, stream)) != MOE_OK) return r;
+    if (slot_out) *slot_out = slot;
+    return MOE_OK;
+}
+
+moe_status moe_quantize_fp8(const void *x_bf16, int32_t T, int32_t d, void *x_q, float *x_s,
+                            void *stream)
+{
+    if (T < 0 || d <= 0 || d % 128) return MOE_EINVAL;
+    if (T > 0 && (!x_bf16 || !x_q || !x_s)) return MOE_EINVAL;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return MOE_EHIP;
+    if (launch_quantize_fp8(x_bf16, T, d, x_q, x_s, cus, (hipStream_t)stream) != hipSuccess)
+        return MOE_EHIP;
+    return MOE_OK;
+}
+
+moe_status moe_stage_query(moe_stage *st, int32_t slot, moe_dispatch_view *v)
+{
+    if (!slot_ok(st, slot) || !v) return MOE_EINVAL;
+    SlotWs &sl = st->slots[slot];
+    v->counts = sl.counts;
+    v->offsets = sl.offsets;
+    v->slot_of_row = sl.slot_of_row;
+    v->row_of_slot = sl.row_of_slot;
+    v->x_perm = sl.x_perm;
+    v->x_perm_scales = sl.x_perm_s;
+    v->h = sl.h;
+    v->h_scales = sl.h_s;
+    v->y_perm = sl.y_perm;
+    v->h_shared = sl.h_sh;
+    v->h_shared_scales = sl.h_sh_s;
+    v->y_shared = sl.y_sh;
+    v->capacity_rows = (int32_t)st->sz.cap;
+    v->n_tokens = sl.has_mb ? sl.mb.n_tokens : 0;
+    return MOE_OK;
+}
+
+moe_status moe_stage_sync(moe_stage *st)
+{
+    if (!st) return MOE_EINVAL;
+    for (auto &sl : st->slots)
+        if (sl.ev_recorded && hipEventSynchronize(sl.ev) != hipSuccess) return MOE_EHIP;
+    int32_t err = 0;
+    if (hipMemcpyAsync(&err, st->err, 4, hipMemcpyDeviceToHost, st->own) != hipSuccess ||
+        hipStreamSynchronize(st->own) != hipSuccess)
+        return MOE_EHIP;
+    if (err) {
+        if (hipMemsetAsync(st->err, 0, 4, st->own) != hipSuccess ||
+            hipStreamSynchronize(st->own) != hipSuccess)
+            return MOE_EHIP;
+        return MOE_EBADID;
+    }
+    return MOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+"""The C-ABI library loads without a GPU and exports every entry point the
+header declares; host-only entry points work on the CPU."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2606_22541_amd import moe_stage as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe_stage.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"MOE_API\s+[\w\s\*]*?\b(moe_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(C.LIB_PATH):
+        from paper_2606_22541_amd import build
+        build.build()
+    return C.load_library()
+
+
+def test_header_and_binding_agree():
+    assert _declared() == sorted(C.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", C.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    assert set(_declared()) <= exported
+    # only the C ABI is exported from the library's own code
+    assert {s for s in exported if s.startswith("moe")} == set(_declared())
+
+
+def test_status_strings(lib):
+    for code in (C.MOE_OK, C.MOE_EINVAL, C.MOE_ENOMEM, C.MOE_EHIP, C.MOE_EBADID,
+                 C.MOE_EUNSUPPORTED, C.MOE_EBUSY):
+        assert C.moe_status_string(code) not in ("", "unknown status")
+    assert C.moe_status_string(12345) == "unknown status"
+
+
+def test_workspace_bytes_host_only(lib):
+    d = C.make_desc(7168, 2048, 256, 0, 8, 8, 32768, n_slots=1)
+    one = C.moe_stage_workspace_bytes(d)
+    d2 = C.make_desc(7168, 2048, 256, 0, 8, 8, 32768, n_slots=3)
+    three = C.moe_stage_workspace_bytes(d2)
+    per_slot = (three - one) // 2
+    weights = one - per_slot
+    # weights: 8 experts x 3 bf16 matrices of 2048 x 7168
+    assert weights >= 8 * 3 * 2048 * 7168 * 2
+    assert weights < 8 * 3 * 2048 * 7168 * 2 + 4096
+    # per slot: X_perm and Y_perm hold T*k rows of d bf16, H holds T*k rows of f
+    rows = 32768 * 8
+    assert per_slot >= rows * (7168 * 2 * 2 + 2048 * 2)
+    fp8 = C.make_desc(7168, 2048, 256, 0, 8, 8, 32768, n_slots=1, dtype=C.MOE_DTYPE_FP8_E4M3_B128)
+    assert C.moe_stage_workspace_bytes(fp8) < one
+
+
+@pytest.mark.parametrize("bad", [
+    dict(d_model=200), dict(d_ff=100), dict(n_experts=0), dict(n_experts=2000),
+    dict(n_local_experts=0), dict(first_local_expert=250), dict(top_k=0), dict(top_k=33),
+    dict(max_tokens=-1), dict(n_slots=0), dict(dtype=7), dict(has_shared_expert=2),
+])
+def test_invalid_desc_rejected(lib, bad):
+    args = dict(d_model=256, d_ff=128, n_experts=8, first_local_expert=0, n_local_experts=4,
+                top_k=2, max_tokens=64, n_slots=1, dtype=0, has_shared_expert=0)
+    args.update(bad)
+    d = C.moe_stage_desc(**args)
+    with pytest.raises(C.MoEStageError) as e:
+        C.moe_stage_workspace_bytes(d)
+    assert e.value.status == C.MOE_EINVAL
+
+
+def test_null_arguments_rejected_without_gpu(lib):
+    assert lib.moe_stage_sync(None) == C.MOE_EINVAL
+    assert lib.moe_dispatch(None, 0, None, None) == C.MOE_EINVAL
+    assert lib.moe_stage_create(None, None, None) == C.MOE_EINVAL
+    lib.moe_stage_destroy(None)

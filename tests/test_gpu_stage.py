@@ -1,0 +1,212 @@
+"""GPU parity of the HIP expert stage against the CPU oracle (bf16 path).
+
+Bit-exact: counts, offsets, slot_of_row, row_of_slot, X_perm.
+Floating point: rel-L2 <= 1e-2 on outputs and per expert on Y_perm rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_22541_amd import inputs
+from paper_2606_22541_amd import moe_stage as C
+from paper_2606_22541_amd.stage import ExpertStage, bf16_bits, to_device_routing
+
+from gpu_common import (BF16_TOL, check_dispatch, check_expert_rows, check_outputs, gpu_run, log,
+                        oracle_run, sample_tokens)
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(cfg, mbs=None, *, n_streams=1, tokens=None, mode=0, tol=BF16_TOL, n_slots=None):
+    log("case %s: d=%d f=%d E=%d E_loc=%d k=%d lengths=%s shared=%d streams=%d" % (
+        cfg.name, cfg.d, cfg.f, cfg.E, cfg.E_loc, cfg.k, cfg.lengths, cfg.has_shared, n_streams))
+    w = inputs.make_weights(cfg, "cuda")
+    if mbs is None:
+        mbs = inputs.make_microbatches(cfg, "cuda")
+    ow = oracle.OracleWeights(w, cfg.dtype)
+    streams = [torch.cuda.Stream() for _ in range(n_streams)] if n_streams > 1 else None
+    with ExpertStage(cfg, w, n_slots=n_slots or len(mbs),
+                     max_tokens=max(max(mb.ids.shape[0] for mb in mbs), 1)) as st:
+        outs, slots, keep = gpu_run(st, mbs, streams=streams, mode=mode)
+        errs = []
+        for mb, ob, sl in zip(mbs, outs, slots):
+            T = mb.ids.shape[0]
+            tok = tokens if tokens is None else sample_tokens(T, tokens)
+            ref = oracle_run(cfg, ow, mb, tokens=tok)
+            view = st.view(sl)
+            check_dispatch(view, ref, cfg, mb)
+            errs.append(check_outputs(ob, ref, tol, cfg.name))
+            check_expert_rows(view, ref, cfg, tol, cfg.name)
+        log("  rel-L2 per micro-batch: %s" % ["%.2e" % e for e in errs])
+    return outs
+
+
+def test_c0_tiny_full_parity():
+    _case(inputs.CONFIGS["c0"])
+
+
+@pytest.mark.parametrize("T,d,f,E,E_loc,k", [
+    (700, 1024, 384, 16, 4, 4),     # several row and column tiles, ragged tails
+    (333, 640, 256, 8, 3, 2),       # d = 640: partial 256-column tile in the down GEMM
+    (1, 256, 128, 8, 4, 2),         # one token
+    (257, 256, 128, 1, 1, 1),       # one expert, 257 rows: tile + 1
+])
+def test_multi_tile_shapes(T, d, f, E, E_loc, k):
+    cfg = inputs.MoEConfig("mt", d=d, f=f, E=E, e0=0, E_loc=E_loc, k=k, lengths=(T,), seed=3)
+    _case(cfg)
+
+
+def test_multi_tile_with_shared_expert_and_offset_experts():
+    cfg = inputs.MoEConfig("sh", d=512, f=256, E=12, e0=5, E_loc=4, k=3, lengths=(600,),
+                           has_shared=True, seed=4)
+    _case(cfg)
+
+
+def test_edge_cases_dispatch_and_outputs():
+    cfg = inputs.MoEConfig("edge", d=256, f=128, E=8, e0=0, E_loc=4, k=2, lengths=(0,), seed=5)
+    w = inputs.make_weights(cfg, "cuda")
+    ow = oracle.OracleWeights(w, "bf16")
+    rng = np.random.default_rng(0)
+    cases = {
+        "empty": np.zeros((0, 2), np.int32),
+        "all_masked": np.full((9, 2), -1, np.int32),
+        "one_expert": np.full((300, 2), 2, np.int32),            # duplicates count twice
+        "tile_minus_one": np.stack([np.full(255, 1), np.full(255, 5)], 1).astype(np.int32),
+        "tile_plus_one": np.stack([np.full(257, 3), np.full(257, -1)], 1).astype(np.int32),
+        "mixed": rng.integers(-1, 8, size=(513, 2)).astype(np.int32),
+    }
+    with ExpertStage(cfg, w, n_slots=2, max_tokens=600) as st:
+        for name, ids in cases.items():
+            log("edge case %s T=%d" % (name, ids.shape[0]))
+            T = ids.shape[0]
+            x = torch.randn((T, cfg.d), generator=torch.Generator("cuda").manual_seed(1),
+                            device="cuda").to(torch.bfloat16)
+            mb = inputs.MicroBatch(x=x, ids=ids, w=rng.random((T, 2)).astype(np.float32))
+            outs, slots, _ = gpu_run(st, [mb])
+            ref = oracle_run(cfg, ow, mb)
+            view = st.view(slots[0])
+            check_dispatch(view, ref, cfg, mb)
+            if T:
+                check_outputs(outs[0], ref, BF16_TOL, name)
+
+
+def test_bad_expert_id_is_reported_and_skipped():
+    cfg = inputs.MoEConfig("bad", d=256, f=128, E=8, e0=0, E_loc=4, k=2, lengths=(5,), seed=6)
+    w = inputs.make_weights(cfg, "cuda")
+    ids = np.array([[0, 1], [9, 2], [-7, 3], [1, -1], [2, 2]], np.int32)
+    mb = inputs.MicroBatch(x=torch.ones((5, 256), dtype=torch.bfloat16, device="cuda"), ids=ids,
+                           w=np.full((5, 2), 0.5, np.float32))
+    with ExpertStage(cfg, w) as st:
+        i, wt = to_device_routing(ids, mb.w)
+        out = torch.zeros((5, 256), dtype=torch.bfloat16, device="cuda")
+        st.submit(st.microbatch(mb.x, i, wt, out))
+        assert C.moe_stage_sync_status(st.handle) == C.MOE_EBADID
+        assert C.moe_stage_sync_status(st.handle) == C.MOE_OK          # reported once
+        view = st.view(0)
+        ref = oracle.dispatch(np.where((ids >= -1) & (ids < 8), ids, -1), 8, 0, 4)
+        assert np.array_equal(view["row_of_slot"], ref["row_of_slot"])
+        assert np.array_equal(view["counts"], ref["counts"])
+
+
+def test_host_errors_enqueue_nothing():
+    cfg = inputs.MoEConfig("err", d=256, f=128, E=8, e0=0, E_loc=4, k=2, lengths=(4,), seed=7)
+    w = inputs.make_weights(cfg, "cuda")
+    with ExpertStage(cfg, w, max_tokens=4) as st:
+        ids, wt = to_device_routing(np.zeros((8, 2), np.int32), np.ones((8, 2), np.float32))
+        x = torch.zeros((8, 256), dtype=torch.bfloat16, device="cuda")
+        out = torch.zeros((8, 256), dtype=torch.bfloat16, device="cuda")
+        with pytest.raises(C.MoEStageError) as e:             # T > max_tokens
+            st.submit(st.microbatch(x, ids, wt, out))
+        assert e.value.status == C.MOE_EINVAL
+        with pytest.raises(C.MoEStageError):                  # bad slot
+            C.moe_dispatch(st.handle, 3, C.make_microbatch(2, x, ids, wt, out))
+        with pytest.raises(C.MoEStageError):                  # null pointer
+            C.moe_dispatch(st.handle, 0, C.make_microbatch(2, None, ids, wt, out))
+        with pytest.raises(C.MoEStageError):                  # ffn before any dispatch
+            C.moe_expert_ffn(st.handle, 0)
+        with pytest.raises(C.MoEStageError):                  # bad combine mode
+            C.moe_dispatch(st.handle, 0, C.make_microbatch(2, x, ids, wt, out, combine_mode=7))
+        assert C.moe_stage_sync_status(st.handle) == C.MOE_OK
+    bad = C.make_desc(200, 128, 8, 0, 4, 2, 4)                # d not a multiple of 128
+    with pytest.raises(C.MoEStageError):
+        C.moe_stage_create(bad, C.make_weights(w.w_gate, w.w_up, w.w_down))
+
+
+def test_accumulate_mode_and_determinism():
+    cfg = inputs.MoEConfig("acc", d=512, f=256, E=16, e0=0, E_loc=4, k=4, lengths=(300,), seed=8)
+    w = inputs.make_weights(cfg, "cuda")
+    mbs = inputs.make_microbatches(cfg, "cuda")
+    ow = oracle.OracleWeights(w, "bf16")
+    base = torch.randn((300, 512), device="cuda").to(torch.bfloat16)
+    with ExpertStage(cfg, w, n_slots=2) as st:
+        o1, s1, _ = gpu_run(st, mbs, mode=C.MOE_COMBINE_ACCUMULATE, out_init=[base])
+        o2, _, _ = gpu_run(st, mbs, mode=C.MOE_COMBINE_ACCUMULATE, out_init=[base])
+        assert np.array_equal(o1[0], o2[0]), "not bit-identical run to run"
+        ref = oracle_run(cfg, ow, mbs[0], mode=1, base=oracle.bf16_bits_to_f64(bf16_bits(base)))
+        check_outputs(o1[0], ref, BF16_TOL, "accumulate")
+        untouched = np.all(ref["row_of_slot"].reshape(300, 4) < 0, axis=1)
+        assert np.array_equal(o1[0][untouched], bf16_bits(base)[untouched])
+
+
+def test_down_weight_scaling_is_exact():
+    """Doubling W_down doubles Y and the output exactly (power-of-two scale)."""
+    cfg = inputs.MoEConfig("x2", d=512, f=256, E=8, e0=0, E_loc=4, k=2, lengths=(200,), seed=9)
+    w = inputs.make_weights(cfg, "cuda")
+    mbs = inputs.make_microbatches(cfg, "cuda")
+    with ExpertStage(cfg, w) as st:
+        o1, _, _ = gpu_run(st, mbs)
+    w.w_down = (w.w_down.float() * 2).to(torch.bfloat16)
+    with ExpertStage(cfg, w) as st:
+        o2, _, _ = gpu_run(st, mbs)
+    a = oracle.bf16_bits_to_f64(o1[0])
+    b = oracle.bf16_bits_to_f64(o2[0])
+    assert np.array_equal(b, 2 * a)
+
+
+def test_empty_experts_poisoned_with_nan_contribute_nothing():
+    cfg = inputs.MoEConfig("nan", d=256, f=128, E=8, e0=0, E_loc=4, k=2, lengths=(100,), seed=10)
+    w = inputs.make_weights(cfg, "cuda")
+    rng = np.random.default_rng(1)
+    ids = np.stack([rng.choice([0, 2, 4, 6, 7], size=2, replace=False) for _ in range(100)]).astype(np.int32)
+    for m in (w.w_gate, w.w_up, w.w_down):
+        m[1].fill_(float("nan"))
+        m[3].fill_(float("nan"))
+    mb = inputs.MicroBatch(x=torch.randn((100, 256), device="cuda").to(torch.bfloat16), ids=ids,
+                           w=rng.random((100, 2)).astype(np.float32))
+    with ExpertStage(cfg, w) as st:
+        outs, _, _ = gpu_run(st, [mb])
+    assert np.all(np.isfinite(oracle.bf16_bits_to_f64(outs[0])))
+
+
+def test_streams_match_single_stream_bitwise():
+    cfg = inputs.scaled(inputs.CONFIGS["c2"], d=512, f=256, name="c2s")
+    w = inputs.make_weights(cfg, "cuda")
+    mbs = inputs.make_microbatches(cfg, "cuda")
+    with ExpertStage(cfg, w, n_slots=4, max_tokens=cfg.max_tokens) as st:
+        one, _, _ = gpu_run(st, mbs)
+        four, _, _ = gpu_run(st, mbs, streams=[torch.cuda.Stream() for _ in range(4)])
+        two_slots = ExpertStage(cfg, w, n_slots=2, max_tokens=cfg.max_tokens)
+        ring, _, _ = gpu_run(two_slots, mbs, streams=[torch.cuda.Stream() for _ in range(4)])
+        two_slots.close()
+    for a, b, c in zip(one, four, ring):
+        assert np.array_equal(a, b) and np.array_equal(a, c)
+
+
+# ---------------------------------------------------------------------------
+# Full-size configurations (outputs checked on sampled tokens)
+# ---------------------------------------------------------------------------
+def test_c1_deepseek_ep32_share():
+    _case(inputs.CONFIGS["c1"], tokens=96)
+
+
+def test_c1p_deepseek_ep32_share_32k_tokens():
+    _case(inputs.CONFIGS["c1p"], tokens=64)
+
+
+def test_c2_skewed_four_streams():
+    _case(inputs.CONFIGS["c2"], n_streams=4, tokens=48)
+
+
+def test_c3_ep8_share_with_shared_expert():
+    _case(inputs.CONFIGS["c3"], tokens=48)
