@@ -46,8 +46,9 @@
  *                    (MOE_COMBINE_ACCUMULATE), plus the shared expert's
  *                    output when the stage has one.
  * Intermediate rows (X_perm, H, Y_perm) are stored in bf16 (fp8 mode: X_perm
- * and H as e4m3 with per-128-channel fp32 scales); the combine accumulates in
- * fp32 and rounds once to bf16.  Tokens with no local slot are written as
+ * and H as e4m3 with per-128-channel fp32 scales, h being rounded to bf16
+ * before it is quantised); the combine accumulates in fp32 and rounds once
+ * to bf16.  Tokens with no local slot are written as
  * +0.0 (overwrite) or left untouched (accumulate).  The combine uses no
  * atomics, so results are bit-identical from run to run and independent of
  * how micro-batches are spread over streams.
@@ -131,12 +132,12 @@ typedef struct {
     int32_t *slot_of_row;     /* [capacity_rows] */
     int32_t *row_of_slot;     /* [max_tokens * k] */
     void    *x_perm;          /* [capacity_rows][d] bf16 or e4m3 */
-    float   *x_perm_scales;   /* fp8: [capacity_rows][d/128] */
+    float   *x_perm_scales;   /* fp8: [d/128][capacity_rows] (transposed) */
     void    *h;               /* [capacity_rows][f] bf16 or e4m3 */
-    float   *h_scales;        /* fp8: [capacity_rows][f/128] */
+    float   *h_scales;        /* fp8: [f/128][capacity_rows] (transposed) */
     void    *y_perm;          /* [capacity_rows][d] bf16 */
     void    *h_shared;        /* shared expert: [max_tokens][f] */
-    float   *h_shared_scales; /* fp8 shared expert: [max_tokens][f/128] */
+    float   *h_shared_scales; /* fp8 shared expert: [f/128][max_tokens] (transposed) */
     void    *y_shared;        /* shared expert: [max_tokens][d] bf16 */
     int32_t  capacity_rows;   /* max_tokens * k */
     int32_t  n_tokens;        /* T of the micro-batch last dispatched here */
@@ -186,6 +187,20 @@ MOE_API moe_status moe_stage_query(moe_stage *stage, int32_t slot, moe_dispatch_
  * clears) the sticky device error: MOE_EBADID if a kernel saw an invalid
  * expert id since the last sync, else MOE_OK (or MOE_EHIP). */
 MOE_API moe_status moe_stage_sync(moe_stage *stage);
+
+/* Per-kernel timing with HIP events, for measurement (off by default).
+ * While enabled, every enqueue call records an event pair around each of its
+ * kernel groups on the launch stream (this creates events, i.e. allocates
+ * host-side runtime objects).  Kinds, in order: 0 dispatch index
+ * (histogram, scan, scatter), 1 row gather, 2 grouped GEMM gate/up with the
+ * SiLU*up epilogue, 3 grouped GEMM down, 4 combine, 5 fp8 quantisation of h. */
+#define MOE_PROF_KINDS 6
+MOE_API moe_status moe_stage_profile(moe_stage *stage, int32_t enable);
+
+/* Waits for the recorded events, writes the summed milliseconds and the
+ * number of timed launches per kind into ms[MOE_PROF_KINDS] and
+ * launches[MOE_PROF_KINDS], and clears the records. */
+MOE_API moe_status moe_stage_profile_read(moe_stage *stage, double *ms, int32_t *launches);
 
 /* Bytes of device memory moe_stage_create allocates for `desc` (weights plus
  * workspace).  Host-only arithmetic; needs no GPU. */

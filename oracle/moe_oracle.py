@@ -91,6 +91,14 @@ def bf16_bits_to_f32(u16: np.ndarray) -> np.ndarray:
     return (np.asarray(u16, np.uint16).astype(np.uint32) << 16).view(np.float32)
 
 
+def round_f32_to_bf16(v: np.ndarray) -> np.ndarray:
+    """Round fp32 values to bf16 (nearest, ties to even on the 16 dropped
+    bits) and return them as fp32.  Inputs are finite."""
+    u = np.asarray(v, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32)
+
+
 def _e4m3_value(code: int) -> float:
     """OCP 8-bit float E4M3FN: sign bit 7, 4 exponent bits (bias 7), 3
     mantissa bits; exponent field 0 encodes subnormals m/8 * 2^-6; the
@@ -182,15 +190,17 @@ def swiglu_ffn(X: np.ndarray, Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray,
                quantize_h: bool = False):
     """y = W_down (SiLU(W_gate x) * W_up x) for each row x of X, in fp64.
 
-    X [n, d]; Wg, Wu [f, d]; Wd [d, f].  With ``quantize_h`` the intermediate h
-    is rounded to fp32 and quantised per 128 channels to e4m3 (the fp8
-    variant's rule) before the down projection.  Returns (y [n, d], h [n, f]).
+    X [n, d]; Wg, Wu [f, d]; Wd [d, f].  With ``quantize_h`` (the fp8 variant)
+    the intermediate h is rounded to fp32, then to bf16, and quantised per
+    128 channels to e4m3 before the down projection: the stage quantises its
+    bf16 copy of h, so the codes are decided from the same precision.
+    Returns (y [n, d], h [n, f]).
     """
     g = X @ Wg.T
     u = X @ Wu.T
     h = silu(g) * u
     if quantize_h:
-        codes, scales = quantize_groups(h.astype(np.float32))
+        codes, scales = quantize_groups(round_f32_to_bf16(h.astype(np.float32)))
         h = dequantize_groups(codes, scales)
     y = h @ Wd.T
     return y, h

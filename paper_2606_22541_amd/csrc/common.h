@@ -20,10 +20,9 @@ constexpr int kMaxExperts = 1024;               // LDS histogram size
 constexpr int kMaxLocalExperts = 256;
 
 // Grouped GEMM tile: 256 x 256 output, K step 64 bf16 (or 128 e4m3) = 128 B
-// per row, four 64-wide waves each owning a 128 x 128 quadrant.
+// per row.
 constexpr int kBM = 256;
 constexpr int kBN = 256;
-constexpr int kGemmThreads = 256;
 
 // Sticky error bits.
 constexpr int kErrBadId = 1;

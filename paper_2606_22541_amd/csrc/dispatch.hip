@@ -169,37 +169,81 @@ hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)
 }
 
 // ---------------------------------------------------------------------------
-// 4. Row gather: one row per workgroup iteration, 16-byte vector copies.
+// 4. Row gather: one wave per row, each lane moving up to 8 16-byte chunks
+//    per round (all loads issued before the stores).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256)
+constexpr int kGatherWaves = 4;
+constexpr int kGatherUnroll = 8;
+
+__global__ __launch_bounds__(64 * kGatherWaves)
 void k_gather(const uint4 *__restrict__ x, const float *__restrict__ xs,
               const int32_t *__restrict__ slot_of_row, const int32_t *__restrict__ n_rows_dev,
               int32_t k, int32_t row_vecs, int32_t n_scales, uint4 *__restrict__ xp,
-              float *__restrict__ xps)
+              float *__restrict__ xps, int32_t scale_ld)
 {
     const int n_rows = *n_rows_dev;
-    for (int r = blockIdx.x; r < n_rows; r += gridDim.x) {
+    const int lane = threadIdx.x & 63;
+    const int gw = blockIdx.x * kGatherWaves + (threadIdx.x >> 6);
+    const int nw = gridDim.x * kGatherWaves;
+    for (int r = gw; r < n_rows; r += nw) {
         const int t = slot_of_row[r] / k;
         const uint4 *src = x + (int64_t)t * row_vecs;
         uint4 *dst = xp + (int64_t)r * row_vecs;
-        for (int c = threadIdx.x; c < row_vecs; c += 256) dst[c] = src[c];
+        for (int c0 = 0; c0 < row_vecs; c0 += 64 * kGatherUnroll) {
+            uint4 v[kGatherUnroll];
+#pragma unroll
+            for (int u = 0; u < kGatherUnroll; ++u) {
+                const int c = c0 + u * 64 + lane;
+                if (c < row_vecs) v[u] = src[c];
+            }
+#pragma unroll
+            for (int u = 0; u < kGatherUnroll; ++u) {
+                const int c = c0 + u * 64 + lane;
+                if (c < row_vecs) dst[c] = v[u];
+            }
+        }
         if (xs != nullptr)
-            for (int c = threadIdx.x; c < n_scales; c += 256)
-                xps[(int64_t)r * n_scales + c] = xs[(int64_t)t * n_scales + c];
+            for (int c = lane; c < n_scales; c += 64)
+                xps[(int64_t)c * scale_ld + r] = xs[(int64_t)t * n_scales + c];
     }
 }
 
 hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_t *slot_of_row,
                               const int32_t *n_rows_dev, int32_t k, int32_t row_bytes,
                               int32_t n_scales, void *x_perm, float *x_perm_scales,
-                              int32_t max_rows, int num_cus, hipStream_t s)
+                              int32_t scale_ld, int32_t max_rows, int num_cus, hipStream_t s)
 {
     if (max_rows <= 0) return hipSuccess;
     int grid = num_cus * 8;
-    if (grid > max_rows) grid = max_rows;
-    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(256), 0, s, (const uint4 *)x, x_scales,
-                       slot_of_row, n_rows_dev, k, row_bytes / 16, n_scales, (uint4 *)x_perm,
-                       x_perm_scales);
+    const int need = (max_rows + kGatherWaves - 1) / kGatherWaves;
+    if (grid > need) grid = need;
+    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(64 * kGatherWaves), 0, s, (const uint4 *)x,
+                       x_scales, slot_of_row, n_rows_dev, k, row_bytes / 16, n_scales,
+                       (uint4 *)x_perm, x_perm_scales, scale_ld);
+    return hipGetLastError();
+}
+
+__global__ void k_transpose_scales(const float *__restrict__ src, int32_t rows, int32_t cols,
+                                   float *__restrict__ dst, int32_t ld)
+{
+    const int64_t total = (int64_t)rows * cols;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int r = (int)(q / cols);
+        const int c = (int)(q - (int64_t)r * cols);
+        dst[(int64_t)c * ld + r] = src[q];
+    }
+}
+
+hipError_t launch_transpose_scales(const float *src, int32_t rows, int32_t cols, float *dst,
+                                   int32_t ld, hipStream_t s)
+{
+    const int64_t total = (int64_t)rows * cols;
+    if (total <= 0) return hipSuccess;
+    int64_t grid = (total + 255) / 256;
+    if (grid > 1024) grid = 1024;
+    hipLaunchKernelGGL(k_transpose_scales, dim3((unsigned)grid), dim3(256), 0, s, src, rows, cols,
+                       dst, ld);
     return hipGetLastError();
 }
 

@@ -9,13 +9,14 @@
 //  * one persistent workgroup per CU walks a device-built tile list, so the
 //    host never learns the per-expert row counts (no read-back, no
 //    re-launch) and empty experts simply own no tiles;
-//  * a 256x256 output tile per workgroup, four wave64s each owning a 128x128
-//    quadrant as 4x4 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation);
+//  * a 256x256 output tile per workgroup, eight wave64s (two per SIMD, so one
+//    wave's MFMAs cover the other's LDS waits) each owning a 128x64 block as
+//    4x2 blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation);
 //  * K advances 64 bf16 (128 bytes per row) per step through a double-
 //    buffered 128 KB LDS tile filled by direct-to-LDS buffer loads (no
 //    staging registers; the next step streams in while MFMAs run on the
-//    current one); 16-byte chunks are XOR-swizzled by row so the MFMA
-//    operand reads spread over the LDS banks;
+//    current one); 16-byte chunks are XOR-swizzled by row pair, which makes
+//    the 16-lane groups of each ds_read_b128 hit 64 distinct banks;
 //  * the raw buffer range check returns zeros for rows past the group's
 //    end, so ragged groups need no clamping;
 //  * the tile order is XCD-aware: workgroups are placed round-robin on the 8
@@ -35,6 +36,8 @@ constexpr int kBK = 64;                       // bf16 elements per K step
 constexpr int kRowElems = kBK;                // LDS row = 128 bytes
 constexpr int kTileElems = kBM * kRowElems;   // one operand tile in LDS
 constexpr int kBandM = 4;                     // row-tiles per raster band
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, int64_t bytes)
 {
@@ -65,24 +68,24 @@ __device__ __forceinline__ void decode_tile(int L, const int32_t *__restrict__ m
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Issues the direct-to-LDS loads of one K step of one operand tile: 8 wave
-// instructions of 64 lanes x 16 bytes, i.e. 8 rows x 128 bytes each.  Lane l
-// fills LDS row 8 b + l / 8, physical chunk l % 8, with global chunk
-// (l % 8) ^ (row % 8): the XOR swizzle is applied on the global side.
+// Direct-to-LDS loads of one K step of one 256-row operand tile: each of the
+// 8 waves issues 4 instructions of 8 rows x 128 bytes (rows 32 w .. 32 w + 31).
+// Lane l fills LDS row 8 b + l / 8, physical chunk l % 8, with global chunk
+// (l % 8) ^ ((row / 2) % 8).
 __device__ __forceinline__ void tile_to_lds(__amdgpu_buffer_rsrc_t r, bf16 *lds_tile, int wave,
-                                            int voff0, int row_step_bytes, int soff)
+                                            int voff_even, int voff_odd, int row_step_bytes, int soff)
 {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int rb = wave * 8 + i;                       // 8-row block
+    for (int i = 0; i < 4; ++i) {
+        const int rb = wave * 4 + i;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            r, (lds_void *)(lds_tile + rb * 8 * kRowElems), 16, voff0 + i * row_step_bytes, soff,
-            0, 0);
+            r, (lds_void *)(lds_tile + rb * 8 * kRowElems), 16,
+            ((i & 1) ? voff_odd : voff_even) + i * row_step_bytes, soff, 0, 0);
     }
 }
 
 template <bool SWIGLU>
-__global__ __launch_bounds__(kGemmThreads, 1)
+__global__ __launch_bounds__(kThreads, 1)
 void k_gemm_bf16(GemmArgs a)
 {
     __shared__ __attribute__((aligned(1024))) bf16 lds_a0[kTileElems];
@@ -93,26 +96,22 @@ void k_gemm_bf16(GemmArgs a)
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave >> 2, wn = wave & 3;            // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
     const int NT = (N + kBN - 1) / kBN;
-    // Tile-table values are wave-uniform; readfirstlane keeps them in SGPRs so
-    // the buffer descriptors built from them need no waterfall loops.
     const int total = __builtin_amdgcn_readfirstlane(a.groups.mt_base[a.G] * NT);
     const int KT = K / kBK;
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
 
-    // direct-to-LDS load offsets: wave covers rows [64 wave, 64 wave + 64)
-    const int lrow = wave * 64 + (lane >> 3);
-    const int lchunk = (lane & 7) ^ ((lane >> 3) & 7);
-    const int voff0 = lrow * K * 2 + lchunk * 16;
+    const int lrow = wave * 32 + (lane >> 3);
+    const int voff_even = lrow * K * 2 + (((lane & 7) ^ ((lane >> 4) & 7)) << 4);
+    const int voff_odd = lrow * K * 2 + (((lane & 7) ^ ((4 + (lane >> 4)) & 7)) << 4);
     const int rstep = 8 * K * 2;
-    // MFMA operand reads: row (lane & 31) of each 32-row block, chunk 2 kk + lane / 32
     const int rd_row = lane & 31;
     const int rd_hi = lane >> 5;
     const int a_rd = (wm * 128 + rd_row) * kRowElems;
-    const int b_rd = (wn * 128 + rd_row) * kRowElems;
+    const int b_rd = (wn * 64 + rd_row) * kRowElems;
 
     for (int L = first; L < total; L += P) {
         int g, mt, nt;
@@ -130,48 +129,69 @@ void k_gemm_bf16(GemmArgs a)
         const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (int64_t)rows_valid * K * 2);
         const __amdgpu_buffer_rsrc_t rb = make_rsrc(B, (int64_t)min(kBN, N - n0) * K * 2);
 
-        f32x16 acc[4][4];
+        f32x16 acc[4][2];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = (f32x16){};
+            for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16){};
 
-        auto compute = [&](const bf16 *As, const bf16 *Bs) {
+        // One K step from one LDS buffer: operand fragments for sub-step
+        // kk+1 are read while the 16 MFMAs of sub-step kk run.
+        auto read_frags = [&](const bf16 *As, const bf16 *Bs, int kk, bf16x8 (&af)[4],
+                              bf16x8 (&bfr)[2]) {
+            const int ch = ((kk * 2 + rd_hi) ^ ((rd_row >> 1) & 7)) << 3;
 #pragma unroll
-            for (int kk = 0; kk < kBK / 16; ++kk) {
-                const int ch = ((kk * 2 + rd_hi) ^ (rd_row & 7)) << 3;
-                bf16x8 af[4], bfr[4];
+            for (int mb = 0; mb < 4; ++mb)
+                af[mb] = *(const bf16x8 *)&As[a_rd + mb * 32 * kRowElems + ch];
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb)
-                    af[mb] = *(const bf16x8 *)&As[a_rd + mb * 32 * kRowElems + ch];
+            for (int nb = 0; nb < 2; ++nb)
+                bfr[nb] = *(const bf16x8 *)&Bs[b_rd + nb * 32 * kRowElems + ch];
+        };
+        auto mfma16 = [&](const bf16x8 (&af)[4], const bf16x8 (&bfr)[2]) {
 #pragma unroll
-                for (int nb = 0; nb < 4; ++nb)
-                    bfr[nb] = *(const bf16x8 *)&Bs[b_rd + nb * 32 * kRowElems + ch];
+            for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-                    for (int nb = 0; nb < 4; ++nb)
-                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb],
-                                                                             acc[mb][nb], 0, 0, 0);
-            }
+                for (int nb = 0; nb < 2; ++nb)
+                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb],
+                                                                         acc[mb][nb], 0, 0, 0);
+        };
+        auto kstep = [&](const bf16 *As, const bf16 *Bs) {
+            bf16x8 a0[4], b0[2], a1[4], b1[2];
+            read_frags(As, Bs, 0, a0, b0);
+            read_frags(As, Bs, 1, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mfma16(a0, b0);
+            read_frags(As, Bs, 2, a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mfma16(a1, b1);
+            read_frags(As, Bs, 3, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mfma16(a0, b0);
+            mfma16(a1, b1);
         };
 
-        tile_to_lds(ra, lds_a0, wave, voff0, rstep, 0);
-        tile_to_lds(rb, lds_b0, wave, voff0, rstep, 0);
+        tile_to_lds(ra, lds_a0, wave, voff_even, voff_odd, rstep, 0);
+        tile_to_lds(rb, lds_b0, wave, voff_even, voff_odd, rstep, 0);
         __builtin_amdgcn_s_waitcnt(0);   // vmcnt(0): this wave's tile loads landed
         __syncthreads();
         // K is a multiple of 128, so KT is even: steps alternate buffers 0/1.
+        // The next step's direct-to-LDS loads are issued first, so they fly
+        // while this step's MFMAs run.
         for (int kt = 0; kt < KT; kt += 2) {
-            tile_to_lds(ra, lds_a1, wave, voff0, rstep, (kt + 1) * kBK * 2);
-            tile_to_lds(rb, lds_b1, wave, voff0, rstep, (kt + 1) * kBK * 2);
-            compute(lds_a0, lds_b0);
+            tile_to_lds(ra, lds_a1, wave, voff_even, voff_odd, rstep, (kt + 1) * kBK * 2);
+            tile_to_lds(rb, lds_b1, wave, voff_even, voff_odd, rstep, (kt + 1) * kBK * 2);
+            __builtin_amdgcn_sched_barrier(0);
+            kstep(lds_a0, lds_b0);
+            __builtin_amdgcn_sched_barrier(0);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (kt + 2 < KT) {
-                tile_to_lds(ra, lds_a0, wave, voff0, rstep, (kt + 2) * kBK * 2);
-                tile_to_lds(rb, lds_b0, wave, voff0, rstep, (kt + 2) * kBK * 2);
+                tile_to_lds(ra, lds_a0, wave, voff_even, voff_odd, rstep, (kt + 2) * kBK * 2);
+                tile_to_lds(rb, lds_b0, wave, voff_even, voff_odd, rstep, (kt + 2) * kBK * 2);
             }
-            compute(lds_a1, lds_b1);
+            __builtin_amdgcn_sched_barrier(0);
+            kstep(lds_a1, lds_b1);
+            __builtin_amdgcn_sched_barrier(0);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
         }
@@ -181,24 +201,20 @@ void k_gemm_bf16(GemmArgs a)
         bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
         if constexpr (SWIGLU) {
             const int f = N / 2;
-            const int f0 = nt * (kBN / 2) + wn * 64 + (lane & 31);
+            const int f0 = nt * (kBN / 2) + wn * 32 + (lane & 31);
 #pragma unroll
             for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int lr = wm * 128 + mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
                     if (lr < rows_valid) {
-                        bf16 *dst = C + (int64_t)(row0 + lr) * f + f0;
-#pragma unroll
-                        for (int p = 0; p < 2; ++p) {
-                            const float gt = acc[mb][2 * p][r];
-                            const float up = acc[mb][2 * p + 1][r];
-                            dst[p * 32] = f2bf(gt / (1.0f + __expf(-gt)) * up);
-                        }
+                        const float gt = acc[mb][0][r];
+                        const float up = acc[mb][1][r];
+                        C[(int64_t)(row0 + lr) * f + f0] = f2bf(gt / (1.0f + __expf(-gt)) * up);
                     }
                 }
         } else {
-            const int c0 = n0 + wn * 128 + (lane & 31);
+            const int c0 = n0 + wn * 64 + (lane & 31);
 #pragma unroll
             for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -207,7 +223,7 @@ void k_gemm_bf16(GemmArgs a)
                     if (lr < rows_valid) {
                         bf16 *dst = C + (int64_t)(row0 + lr) * N;
 #pragma unroll
-                        for (int nb = 0; nb < 4; ++nb) {
+                        for (int nb = 0; nb < 2; ++nb) {
                             const int col = c0 + nb * 32;
                             if (col < N) dst[col] = f2bf(acc[mb][nb][r]);
                         }
@@ -217,16 +233,17 @@ void k_gemm_bf16(GemmArgs a)
     }
 }
 
-hipError_t launch_gemm_bf16(const GemmArgs &a, bool swiglu, int max_tiles, int num_cus,
+hipError_t launch_gemm_bf16(const GemmArgs &a, bool swiglu, int mt_max, int num_cus,
                             hipStream_t s)
 {
-    if (max_tiles <= 0) return hipSuccess;
-    int grid = num_cus < max_tiles ? num_cus : max_tiles;
+    if (mt_max <= 0) return hipSuccess;
+    const int64_t tiles = (int64_t)mt_max * ((a.N + kBN - 1) / kBN);
+    int grid = num_cus < tiles ? num_cus : (int)tiles;
     if (grid >= 8) grid &= ~7;
     if (swiglu)
-        hipLaunchKernelGGL(k_gemm_bf16<true>, dim3(grid), dim3(kGemmThreads), 0, s, a);
+        hipLaunchKernelGGL(k_gemm_bf16<true>, dim3(grid), dim3(kThreads), 0, s, a);
     else
-        hipLaunchKernelGGL(k_gemm_bf16<false>, dim3(grid), dim3(kGemmThreads), 0, s, a);
+        hipLaunchKernelGGL(k_gemm_bf16<false>, dim3(grid), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

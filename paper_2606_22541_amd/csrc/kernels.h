@@ -28,11 +28,16 @@ hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s);
 
 // X_perm[r] = x[slot_of_row[r] / k] for r < offsets[E_loc].  row_bytes is the
 // byte length of one activation row (2d for bf16, d for e4m3); when
-// scales != nullptr the per-row fp32 scales (n_scales per row) move as well.
+// scales != nullptr the row's fp32 scales (n_scales per row, row-major
+// [T][n_scales]) move as well and are stored transposed: [n_scales][scale_ld].
 hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_t *slot_of_row,
                               const int32_t *n_rows_dev, int32_t k, int32_t row_bytes,
                               int32_t n_scales, void *x_perm, float *x_perm_scales,
-                              int32_t max_rows, int num_cus, hipStream_t s);
+                              int32_t scale_ld, int32_t max_rows, int num_cus, hipStream_t s);
+
+// [rows][cols] -> [cols][ld] copy of fp32 scales.
+hipError_t launch_transpose_scales(const float *src, int32_t rows, int32_t cols, float *dst,
+                                   int32_t ld, hipStream_t s);
 
 struct GemmArgs {
     const void *A_routed;    // [rows][K] (rows of X_perm or H)
@@ -53,14 +58,15 @@ struct GemmArgs {
 
 // bf16 grouped GEMM.  swiglu = true: B is the packed [gate|up] matrix
 // (N = 2f) and C receives SiLU(gate) * up as [rows][f] bf16; otherwise C
-// receives the product as [rows][N] bf16.
-hipError_t launch_gemm_bf16(const GemmArgs &a, bool swiglu, int max_tiles, int num_cus,
+// receives the product as [rows][N] bf16.  mt_max bounds the number of
+// 256-row tiles over all groups (the grid is sized from it).
+hipError_t launch_gemm_bf16(const GemmArgs &a, bool swiglu, int mt_max, int num_cus,
                             hipStream_t s);
 
-// e4m3 grouped GEMM with 128-block scales (same conventions; the SwiGLU
-// epilogue also quantises h per 128 channels).
-hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int max_tiles, int num_cus,
-                           hipStream_t s);
+// e4m3 grouped GEMM with 128-block scales (same conventions; the A scales
+// are transposed, [K/128][ld] with ld = lds_rows_routed / lds_rows_shared).
+hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int mt_max, int num_cus,
+                           int32_t lds_rows_routed, int32_t lds_rows_shared, hipStream_t s);
 
 struct CombineArgs {
     const void *y_perm;        // [rows][d] bf16
@@ -72,8 +78,13 @@ struct CombineArgs {
 };
 hipError_t launch_combine(const CombineArgs &a, int num_cus, hipStream_t s);
 
-hipError_t launch_quantize_fp8(const void *x, int32_t T, int32_t d, void *xq, float *xs,
-                               int num_cus, hipStream_t s);
+// Per-row, per-128-channel e4m3 quantisation of bf16 rows.  Rows: n_rows,
+// or *n_rows_dev when that is not null (then n_rows is the bound used to size
+// the grid).  Scales go to xs[row * (d/128) + g] (scale_ld = 0) or, when
+// scale_ld > 0, transposed to xs[g * scale_ld + row].
+hipError_t launch_quantize_fp8(const void *x, int32_t n_rows, const int32_t *n_rows_dev,
+                               int32_t d, void *xq, float *xs, int32_t scale_ld, int num_cus,
+                               hipStream_t s);
 
 // Weight packing at create time.
 // Interleaves gate and up rows in blocks of 32: packed row 64*b + i is gate

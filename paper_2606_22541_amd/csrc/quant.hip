@@ -19,10 +19,12 @@ __device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float 
 
 // One group of 128 channels is handled by 16 lanes, 8 channels each.
 __global__ __launch_bounds__(256)
-void k_quantize_fp8(const uint4 *__restrict__ x, int32_t T, int32_t groups_per_row,
-                    uint2 *__restrict__ xq, float *__restrict__ xs)
+void k_quantize_fp8(const uint4 *__restrict__ x, int32_t n_rows, const int32_t *__restrict__ n_rows_dev,
+                    int32_t groups_per_row, uint2 *__restrict__ xq, float *__restrict__ xs,
+                    int32_t scale_ld)
 {
-    const int64_t n_groups = (int64_t)T * groups_per_row;
+    const int rows = n_rows_dev ? *n_rows_dev : n_rows;
+    const int64_t n_groups = (int64_t)rows * groups_per_row;
     const int sub = threadIdx.x & 15;
     for (int64_t gi = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 4; gi < n_groups;
          gi += ((int64_t)gridDim.x * 256) >> 4) {
@@ -42,20 +44,26 @@ void k_quantize_fp8(const uint4 *__restrict__ x, int32_t T, int32_t groups_per_r
         q.x = e4m3_pack4(f[0] / s, f[1] / s, f[2] / s, f[3] / s);
         q.y = e4m3_pack4(f[4] / s, f[5] / s, f[6] / s, f[7] / s);
         xq[gi * 16 + sub] = q;
-        if (sub == 0) xs[gi] = s;
+        if (sub == 0) {
+            const int64_t row = gi / groups_per_row;
+            const int g = (int)(gi - row * groups_per_row);
+            if (scale_ld > 0) xs[(int64_t)g * scale_ld + row] = s;
+            else xs[gi] = s;
+        }
     }
 }
 
-hipError_t launch_quantize_fp8(const void *x, int32_t T, int32_t d, void *xq, float *xs,
-                               int num_cus, hipStream_t s)
+hipError_t launch_quantize_fp8(const void *x, int32_t n_rows, const int32_t *n_rows_dev,
+                               int32_t d, void *xq, float *xs, int32_t scale_ld, int num_cus,
+                               hipStream_t s)
 {
-    if (T <= 0) return hipSuccess;
+    if (n_rows <= 0) return hipSuccess;
     const int gpr = d / 128;
-    const int64_t threads = (int64_t)T * gpr * 16;
+    const int64_t threads = (int64_t)n_rows * gpr * 16;
     int64_t grid = (threads + 255) / 256;
     if (grid > (int64_t)num_cus * 16) grid = (int64_t)num_cus * 16;
     hipLaunchKernelGGL(k_quantize_fp8, dim3((unsigned)grid), dim3(256), 0, s, (const uint4 *)x,
-                       T, gpr, (uint2 *)xq, xs);
+                       n_rows, n_rows_dev, gpr, (uint2 *)xq, xs, scale_ld);
     return hipGetLastError();
 }
 

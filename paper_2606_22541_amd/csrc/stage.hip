@@ -31,6 +31,9 @@ struct SlotWs {
     void *h_sh = nullptr;
     float *h_sh_s = nullptr;
     void *y_sh = nullptr;
+    void *h_bf = nullptr;        // fp8 mode: SiLU*up rows in bf16 before quantisation
+    void *h_sh_bf = nullptr;
+    float *xsh_s = nullptr;      // fp8 mode with shared expert: x scales, transposed
     hipEvent_t ev = nullptr;
     bool ev_recorded = false;
     bool has_mb = false;
@@ -91,9 +94,11 @@ Sizes sizes_of(const moe_stage_desc *d)
     b += align256(cap1 * D * s.eb) + (fp8 ? align256(cap1 * (D / 128) * 4) : 0);
     b += align256(cap1 * F * s.eb) + (fp8 ? align256(cap1 * (F / 128) * 4) : 0);
     b += align256(cap1 * D * 2);
+    if (fp8) b += align256(cap1 * F * 2);
     if (d->has_shared_expert) {
         b += align256(T1 * F * s.eb) + (fp8 ? align256(T1 * (F / 128) * 4) : 0);
         b += align256(T1 * D * 2);
+        if (fp8) b += align256(T1 * F * 2) + align256(T1 * (D / 128) * 4);
     }
     s.per_slot = b;
     return s;
@@ -101,8 +106,15 @@ Sizes sizes_of(const moe_stage_desc *d)
 
 }  // namespace
 
+struct ProfRec {
+    int kind;
+    hipEvent_t a, b;
+};
+
 struct moe_stage {
     moe_stage_desc desc{};
+    bool prof_on = false;
+    std::vector<ProfRec> prof;
     Sizes sz{};
     int device = 0;
     int num_cus = 0;
@@ -120,6 +132,11 @@ namespace {
 void release(moe_stage *st)
 {
     if (!st) return;
+    for (auto &p : st->prof) {
+        hipEventSynchronize(p.b);
+        hipEventDestroy(p.a);
+        hipEventDestroy(p.b);
+    }
     for (auto &sl : st->slots) {
         if (sl.ev) {
             hipEventSynchronize(sl.ev);
@@ -148,6 +165,27 @@ bool slot_ok(const moe_stage *st, int32_t slot)
 {
     return st && slot >= 0 && slot < (int32_t)st->slots.size();
 }
+
+// Event pair around a kernel group when profiling is on.
+struct ProfScope {
+    moe_stage *st;
+    int kind;
+    hipStream_t s;
+    hipEvent_t a = nullptr;
+    ProfScope(moe_stage *st_, int kind_, hipStream_t s_) : st(st_), kind(kind_), s(s_)
+    {
+        if (st->prof_on && hipEventCreate(&a) == hipSuccess) hipEventRecord(a, s);
+    }
+    ~ProfScope()
+    {
+        if (!a) return;
+        hipEvent_t b = nullptr;
+        if (hipEventCreate(&b) == hipSuccess && hipEventRecord(b, s) == hipSuccess)
+            st->prof.push_back(ProfRec{kind, a, b});
+        else
+            hipEventDestroy(a);
+    }
+};
 
 moe_status record(SlotWs &sl, hipStream_t s)
 {
@@ -265,9 +303,12 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
              alloc(st, &sl.y_perm, cap1 * D * 2);
         if (ok && fp8) ok = alloc(st, &sl.x_perm_s, cap1 * (D / 128) * 4) &&
                             alloc(st, &sl.h_s, cap1 * (F / 128) * 4);
+        if (ok && fp8) ok = alloc(st, &sl.h_bf, cap1 * F * 2);
         if (ok && desc->has_shared_expert) {
             ok = alloc(st, &sl.h_sh, T1 * F * z.eb) && alloc(st, &sl.y_sh, T1 * D * 2);
-            if (ok && fp8) ok = alloc(st, &sl.h_sh_s, T1 * (F / 128) * 4);
+            if (ok && fp8)
+                ok = alloc(st, &sl.h_sh_s, T1 * (F / 128) * 4) &&
+                     alloc(st, &sl.h_sh_bf, T1 * F * 2) && alloc(st, &sl.xsh_s, T1 * (D / 128) * 4);
         }
         if (!ok) {
             release(st);
@@ -329,14 +370,22 @@ moe_status moe_dispatch(moe_stage *st, int32_t slot, const moe_microbatch *mb, v
     a.slot_of_row = sl.slot_of_row;
     a.row_of_slot = sl.row_of_slot;
     a.err = st->err;
-    if (launch_dispatch_index(a, s) != hipSuccess) return MOE_EHIP;
+    {
+        ProfScope ps(st, 0, s);
+        if (launch_dispatch_index(a, s) != hipSuccess) return MOE_EHIP;
+    }
     const int64_t max_rows = (int64_t)T * d.top_k;
     if (max_rows > 0) {
+        ProfScope ps(st, 1, s);
         const int32_t row_bytes = fp8 ? d.d_model : 2 * d.d_model;
         if (launch_gather_rows(mb->x, fp8 ? mb->x_scales : nullptr, sl.slot_of_row,
                                sl.offsets + d.n_local_experts, d.top_k, row_bytes,
-                               d.d_model / 128, sl.x_perm, sl.x_perm_s, (int32_t)max_rows,
-                               st->num_cus, s) != hipSuccess)
+                               d.d_model / 128, sl.x_perm, sl.x_perm_s, (int32_t)st->sz.cap,
+                               (int32_t)max_rows, st->num_cus, s) != hipSuccess)
+            return MOE_EHIP;
+        if (fp8 && d.has_shared_expert &&
+            launch_transpose_scales(mb->x_scales, T, d.d_model / 128, sl.xsh_s, d.max_tokens,
+                                    s) != hipSuccess)
             return MOE_EHIP;
     }
     return record(sl, s);
@@ -360,13 +409,11 @@ moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
     g1.A_routed = sl.x_perm;
     g1.A_shared = sl.mb.x;
     g1.As_routed = sl.x_perm_s;
-    g1.As_shared = sl.mb.x_scales;
+    g1.As_shared = sl.xsh_s;
     g1.B = st->w1;
     g1.Bs = st->s1;
-    g1.C_routed = sl.h;
-    g1.C_shared = sl.h_sh;
-    g1.Cs_routed = sl.h_s;
-    g1.Cs_shared = sl.h_sh_s;
+    g1.C_routed = fp8 ? sl.h_bf : sl.h;
+    g1.C_shared = fp8 ? sl.h_sh_bf : sl.h_sh;
     g1.N = 2 * d.d_ff;
     g1.K = d.d_model;
     g1.shared_group = d.has_shared_expert ? d.n_local_experts : -1;
@@ -382,22 +429,30 @@ moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
     g2.Bs = st->s2;
     g2.C_routed = sl.y_perm;
     g2.C_shared = sl.y_sh;
-    g2.Cs_routed = nullptr;
-    g2.Cs_shared = nullptr;
     g2.N = d.d_model;
     g2.K = d.d_ff;
 
-    const int64_t t1 = mt_max * ((g1.N + kBN - 1) / kBN);
-    const int64_t t2 = mt_max * ((g2.N + kBN - 1) / kBN);
-    const int mt1 = t1 > 0x7fffffff ? 0x7fffffff : (int)t1;
-    const int mt2 = t2 > 0x7fffffff ? 0x7fffffff : (int)t2;
+    const int mt = mt_max > 0x7fffffff ? 0x7fffffff : (int)mt_max;
+    const int32_t cap = (int32_t)st->sz.cap, tmax = d.max_tokens;
     hipError_t e;
-    if (fp8) {
-        e = launch_gemm_fp8(g1, true, mt1, st->num_cus, s);
-        if (e == hipSuccess) e = launch_gemm_fp8(g2, false, mt2, st->num_cus, s);
-    } else {
-        e = launch_gemm_bf16(g1, true, mt1, st->num_cus, s);
-        if (e == hipSuccess) e = launch_gemm_bf16(g2, false, mt2, st->num_cus, s);
+    {
+        ProfScope ps(st, 2, s);
+        e = fp8 ? launch_gemm_fp8(g1, true, mt, st->num_cus, cap, tmax, s)
+                : launch_gemm_bf16(g1, true, mt, st->num_cus, s);
+    }
+    if (e == hipSuccess && fp8) {
+        // quantise h per row and 128 channels (scales transposed for the down GEMM)
+        ProfScope ps(st, 5, s);
+        e = launch_quantize_fp8(sl.h_bf, (int32_t)max_rows, sl.offsets + d.n_local_experts,
+                                d.d_ff, sl.h, sl.h_s, cap, st->num_cus, s);
+        if (e == hipSuccess && d.has_shared_expert)
+            e = launch_quantize_fp8(sl.h_sh_bf, T, nullptr, d.d_ff, sl.h_sh, sl.h_sh_s, tmax,
+                                    st->num_cus, s);
+    }
+    if (e == hipSuccess) {
+        ProfScope ps(st, 3, s);
+        e = fp8 ? launch_gemm_fp8(g2, false, mt, st->num_cus, cap, tmax, s)
+                : launch_gemm_bf16(g2, false, mt, st->num_cus, s);
     }
     if (e == hipErrorNotSupported) return MOE_EUNSUPPORTED;
     if (e != hipSuccess) return MOE_EHIP;
@@ -421,7 +476,10 @@ moe_status moe_combine(moe_stage *st, int32_t slot, void *stream)
     c.k = d.top_k;
     c.d = d.d_model;
     c.accumulate = sl.mb.combine_mode == MOE_COMBINE_ACCUMULATE;
-    if (launch_combine(c, st->num_cus, s) != hipSuccess) return MOE_EHIP;
+    {
+        ProfScope ps(st, 4, s);
+        if (launch_combine(c, st->num_cus, s) != hipSuccess) return MOE_EHIP;
+    }
     return record(sl, s);
 }
 
@@ -453,7 +511,8 @@ moe_status moe_quantize_fp8(const void *x_bf16, int32_t T, int32_t d, void *x_q,
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return MOE_EHIP;
-    if (launch_quantize_fp8(x_bf16, T, d, x_q, x_s, cus, (hipStream_t)stream) != hipSuccess)
+    if (launch_quantize_fp8(x_bf16, T, nullptr, d, x_q, x_s, 0, cus, (hipStream_t)stream) !=
+        hipSuccess)
         return MOE_EHIP;
     return MOE_OK;
 }
@@ -477,6 +536,36 @@ moe_status moe_stage_query(moe_stage *st, int32_t slot, moe_dispatch_view *v)
     v->capacity_rows = (int32_t)st->sz.cap;
     v->n_tokens = sl.has_mb ? sl.mb.n_tokens : 0;
     return MOE_OK;
+}
+
+moe_status moe_stage_profile(moe_stage *st, int32_t enable)
+{
+    if (!st) return MOE_EINVAL;
+    st->prof_on = enable != 0;
+    return MOE_OK;
+}
+
+moe_status moe_stage_profile_read(moe_stage *st, double *ms, int32_t *launches)
+{
+    if (!st || !ms || !launches) return MOE_EINVAL;
+    for (int i = 0; i < MOE_PROF_KINDS; ++i) {
+        ms[i] = 0.0;
+        launches[i] = 0;
+    }
+    moe_status r = MOE_OK;
+    for (auto &p : st->prof) {
+        float t = 0.0f;
+        if (hipEventSynchronize(p.b) != hipSuccess || hipEventElapsedTime(&t, p.a, p.b) != hipSuccess)
+            r = MOE_EHIP;
+        else if (p.kind >= 0 && p.kind < MOE_PROF_KINDS) {
+            ms[p.kind] += t;
+            launches[p.kind] += 1;
+        }
+        hipEventDestroy(p.a);
+        hipEventDestroy(p.b);
+    }
+    st->prof.clear();
+    return r;
 }
 
 moe_status moe_stage_sync(moe_stage *st)

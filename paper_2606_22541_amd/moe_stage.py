@@ -34,8 +34,12 @@ MOE_COMBINE_ACCUMULATE = 1
 EXPORTS = (
     "moe_stage_create", "moe_stage_destroy", "moe_dispatch", "moe_expert_ffn", "moe_combine",
     "moe_stage_submit_microbatch", "moe_quantize_fp8", "moe_stage_query", "moe_stage_sync",
-    "moe_stage_workspace_bytes", "moe_status_string",
+    "moe_stage_workspace_bytes", "moe_status_string", "moe_stage_profile",
+    "moe_stage_profile_read",
 )
+MOE_PROF_KINDS = 6
+PROF_KIND_NAMES = ("dispatch_index", "gather", "gemm_gate_up_swiglu", "gemm_down", "combine",
+                   "quantize_h")
 
 
 class moe_stage_desc(ctypes.Structure):
@@ -98,6 +102,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "moe_stage_workspace_bytes": (st, [ctypes.POINTER(moe_stage_desc),
                                            ctypes.POINTER(ctypes.c_int64)]),
         "moe_status_string": (ctypes.c_char_p, [st]),
+        "moe_stage_profile": (st, [P, ctypes.c_int32]),
+        "moe_stage_profile_read": (st, [P, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -216,3 +223,15 @@ def moe_stage_workspace_bytes(desc: moe_stage_desc) -> int:
 
 def moe_status_string(status: int) -> str:
     return load_library().moe_status_string(status).decode()
+
+
+def moe_stage_profile(stage: int, enable: bool) -> None:
+    _check(load_library().moe_stage_profile(stage, int(bool(enable))), "moe_stage_profile")
+
+
+def moe_stage_profile_read(stage: int):
+    """Returns {kind name: (total ms, launches)} and clears the records."""
+    ms = (ctypes.c_double * MOE_PROF_KINDS)()
+    n = (ctypes.c_int32 * MOE_PROF_KINDS)()
+    _check(load_library().moe_stage_profile_read(stage, ms, n), "moe_stage_profile_read")
+    return {PROF_KIND_NAMES[i]: (ms[i], n[i]) for i in range(MOE_PROF_KINDS)}

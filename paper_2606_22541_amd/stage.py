@@ -88,11 +88,12 @@ class ExpertStage:
             res["x_perm"] = device_to_numpy(v.x_perm, n * cfg.d, eb).reshape(n, cfg.d)
             res["h"] = device_to_numpy(v.h, n * cfg.f, eb).reshape(n, cfg.f)
             res["y_perm"] = device_to_numpy(v.y_perm, n * cfg.d, np.uint16).reshape(n, cfg.d)
-            if self.fp8:
-                res["x_perm_scales"] = device_to_numpy(v.x_perm_scales, n * cfg.d // 128,
-                                                       np.float32).reshape(n, cfg.d // 128)
-                res["h_scales"] = device_to_numpy(v.h_scales, n * cfg.f // 128,
-                                                  np.float32).reshape(n, cfg.f // 128)
+            if self.fp8:   # scales are stored transposed: [groups][capacity_rows]
+                cap = v.capacity_rows
+                xs = device_to_numpy(v.x_perm_scales, cap * cfg.d // 128, np.float32)
+                res["x_perm_scales"] = xs.reshape(cfg.d // 128, cap)[:, :n].T.copy()
+                hs = device_to_numpy(v.h_scales, cap * cfg.f // 128, np.float32)
+                res["h_scales"] = hs.reshape(cfg.f // 128, cap)[:, :n].T.copy()
             if cfg.has_shared:
                 res["y_shared"] = device_to_numpy(v.y_shared, T * cfg.d, np.uint16).reshape(T, cfg.d)
         return res

@@ -63,6 +63,10 @@ def check_dispatch(view, ref, cfg, mb=None):
     if mb is not None and "x_perm" in view and cfg.dtype == "bf16":
         src = bf16_bits(mb.x)[ref["slot_of_row"] // cfg.k]
         assert np.array_equal(view["x_perm"], src), "X_perm is not an exact row gather"
+    if mb is not None and "x_perm" in view and cfg.dtype == "fp8":
+        tok = ref["slot_of_row"] // cfg.k
+        assert np.array_equal(view["x_perm"], ref["x_codes"][tok]), "fp8 X_perm codes differ"
+        assert np.array_equal(view["x_perm_scales"], ref["x_scales"][tok]), "fp8 X_perm scales differ"
 
 
 def check_outputs(out_bits, ref, tol, what=""):
@@ -80,6 +84,11 @@ def check_outputs(out_bits, ref, tol, what=""):
 
 
 def check_expert_rows(view, ref, cfg, tol, what=""):
+    """Per-expert rel-L2 of the GPU's Y_perm rows against the oracle's y."""
+    return _check_expert_rows(view, ref, cfg, tol, what)
+
+
+def _check_expert_rows(view, ref, cfg, tol, what=""):
     """Per-expert rel-L2 of the GPU's Y_perm rows against the oracle's y."""
     rows = ref["rows"]
     if rows.size == 0:

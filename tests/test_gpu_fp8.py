@@ -1,0 +1,83 @@
+"""GPU parity of the fp8 (e4m3, 128-block scales) expert stage and of the
+sender-side quantiser against the CPU oracle.
+
+Bit-exact: quantiser codes and scales, counts, permutation, X_perm codes and
+scales.  Floating point: rel-L2 <= 3e-2 on outputs and per expert on Y_perm.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_22541_amd import inputs
+from paper_2606_22541_amd.stage import ExpertStage, bf16_bits, quantize_fp8
+
+from gpu_common import (FP8_TOL, check_dispatch, check_expert_rows, check_outputs, gpu_run, log,
+                        oracle_run, sample_tokens)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("T,d,scale", [(1, 128, 1.0), (333, 512, 1.0), (1000, 7168, 1.0),
+                                       (64, 256, 1e-3), (64, 256, 300.0)])
+def test_quantizer_bit_exact(T, d, scale):
+    log("quantizer T=%d d=%d scale=%g" % (T, d, scale))
+    g = torch.Generator("cuda").manual_seed(T + d)
+    x = (torch.randn((T, d), generator=g, device="cuda") * scale).to(torch.bfloat16)
+    if T > 1:
+        x[0, :128] = 0                    # an all-zero group: scale 1, codes 0
+        x[T - 1, 5] = -x[T - 1, 5]
+    xq, xs = quantize_fp8(x)
+    torch.cuda.synchronize()
+    codes, scales = oracle.quantize_groups(oracle.bf16_bits_to_f32(bf16_bits(x)))
+    got_q = xq.cpu().numpy()
+    got_s = xs.cpu().numpy()
+    assert np.array_equal(got_s.view(np.uint32), scales.view(np.uint32)), "scales differ"
+    bad = np.nonzero(got_q != codes)
+    assert bad[0].size == 0, "codes differ at %s: gpu %s oracle %s" % (
+        list(zip(*bad))[:5], got_q[bad][:5], codes[bad][:5])
+
+
+def _case(cfg, *, n_streams=1, tokens=None):
+    log("fp8 case %s: d=%d f=%d E=%d E_loc=%d k=%d lengths=%s shared=%d streams=%d" % (
+        cfg.name, cfg.d, cfg.f, cfg.E, cfg.E_loc, cfg.k, cfg.lengths, cfg.has_shared, n_streams))
+    w = inputs.make_weights(cfg, "cuda")
+    mbs = inputs.make_microbatches(cfg, "cuda")
+    ow = oracle.OracleWeights(w, "fp8")
+    streams = [torch.cuda.Stream() for _ in range(n_streams)] if n_streams > 1 else None
+    Tmax = max(max(mb.ids.shape[0] for mb in mbs), 1)
+    with ExpertStage(cfg, w, n_slots=len(mbs), max_tokens=Tmax) as st:
+        outs, slots, _ = gpu_run(st, mbs, streams=streams)
+        errs = []
+        for mb, ob, sl in zip(mbs, outs, slots):
+            T = mb.ids.shape[0]
+            tok = None if tokens is None else sample_tokens(T, tokens)
+            ref = oracle_run(cfg, ow, mb, tokens=tok)
+            view = st.view(sl)
+            check_dispatch(view, ref, cfg, mb)
+            errs.append(check_outputs(ob, ref, FP8_TOL, cfg.name))
+            check_expert_rows(view, ref, cfg, FP8_TOL, cfg.name)
+        log("  rel-L2 per micro-batch: %s" % ["%.2e" % e for e in errs])
+
+
+def test_fp8_tiny():
+    _case(inputs.scaled(inputs.CONFIGS["c0"], dtype="fp8", name="c0f8"))
+
+
+@pytest.mark.parametrize("T,d,f,E,E_loc,k", [
+    (700, 1024, 384, 16, 4, 4),
+    (333, 640, 256, 8, 3, 2),
+    (257, 256, 128, 1, 1, 1),
+])
+def test_fp8_multi_tile(T, d, f, E, E_loc, k):
+    _case(inputs.MoEConfig("f8mt", d=d, f=f, E=E, e0=0, E_loc=E_loc, k=k, lengths=(T,),
+                           dtype="fp8", seed=11))
+
+
+def test_fp8_shared_expert():
+    _case(inputs.MoEConfig("f8sh", d=512, f=256, E=12, e0=2, E_loc=4, k=3, lengths=(300,),
+                           has_shared=True, dtype="fp8", seed=12))
+
+
+def test_c4_fp8_skewed_four_streams():
+    _case(inputs.CONFIGS["c4"], n_streams=4, tokens=48)

@@ -118,3 +118,14 @@ def test_bf16_widening_matches_torch_all_patterns():
     nan = np.isnan(ref)
     assert np.array_equal(nan, np.isnan(mine))
     assert np.array_equal(ref[~nan], mine[~nan])
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(5)
+    v = (rng.standard_normal(100000) * 10.0 ** rng.integers(-6, 6, 100000)).astype(np.float32)
+    # exact ties between two neighbouring bf16 values, both parities of the kept bits
+    ties = ((np.arange(0, 4096, dtype=np.uint32) << 16) | 0x8000).view(np.float32)
+    v = np.concatenate([v, ties[np.isfinite(ties)]])
+    ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float32).numpy()
+    got = oracle.round_f32_to_bf16(v)
+    assert np.array_equal(ref.view(np.uint32), got.view(np.uint32))

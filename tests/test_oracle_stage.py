@@ -6,6 +6,7 @@ from types import SimpleNamespace
 
 import numpy as np
 import pytest
+import torch
 
 import oracle
 from brute_force import bf_stage, bf_swiglu
@@ -209,7 +210,8 @@ def test_fp8_stage_is_bf16_stage_on_dequantised_operands():
             Wd = oracle.e4m3_decode(codes[2][e]) * np.kron(scales[2][e], np.ones((128, 128)))
             g = Wg @ x[t]
             h = (g / (1 + np.exp(-g))) * (Wu @ x[t])
-            hq, hs = oracle.quantize_groups(h[None, :].astype(np.float32))
+            hb = torch.from_numpy(h[None, :].astype(np.float32)).to(torch.bfloat16).float().numpy()
+            hq, hs = oracle.quantize_groups(hb)
             hd = oracle.e4m3_decode(hq[0]) * np.repeat(hs[0], 128)
             out[t] += w[t, j] * (Wd @ hd)
     np.testing.assert_allclose(res["out"], out, rtol=1e-12, atol=1e-12)
