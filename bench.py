@@ -121,6 +121,20 @@ def run_workload(name, steps, warmup, n_buffers=3):
                 n_local_slots=int(counts_local.sum()))
 
 
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when it is missing or the kernel's sources changed since."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        from paper_2606_22541_amd.profiling import sources_digest
+        rec = json.load(open(path))["kernels"]["%s:%s" % (workload, kernel)]
+        if rec["source_sha256"] != sources_digest(kernel):
+            return None
+        return rec["bytes_per_dispatch"]
+    except Exception:
+        return None
+
+
 def roofline_for(r, kernel="gemm_gate_up_swiglu"):
     a = r["acct"]
     t = r["kern"][kernel] / 1e3
@@ -132,11 +146,13 @@ def roofline_for(r, kernel="gemm_gate_up_swiglu"):
     if t_mfma >= t_hbm:
         ach = flop / t / 1e12
         return {"kernel": kernel, "bound": "mfma", "achieved": round(ach, 1), "peak": peak_tf,
-                "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4), "traffic": None,
+                "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4),
+                "traffic": measured_traffic(r["cfg"].name, kernel),
                 "algorithmic_flop": flop, "algorithmic_bytes": byts, "avg_ms": round(t * 1e3, 4)}
     ach = byts / t / 1e9
     return {"kernel": kernel, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
-            "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+            "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
+            "traffic": measured_traffic(r["cfg"].name, kernel),
             "algorithmic_flop": flop, "algorithmic_bytes": byts, "avg_ms": round(t * 1e3, 4),
             "tflops": round(flop / t / 1e12, 1)}
 
@@ -204,6 +220,8 @@ def main():
     ap.add_argument("--workload", default="c1")
     ap.add_argument("--secondary", default="c1p", help="'' to skip")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU's expert share; runs on %d GPUs are not part of this "
@@ -213,6 +231,15 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes": n}))
+        return
 
     prim = run_workload(args.workload, args.steps, args.warmup)
     cfg = prim["cfg"]

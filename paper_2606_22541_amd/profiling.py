@@ -1,0 +1,155 @@
+"""Summaries of rocprofv3 output for the stage's kernels.
+
+``kernel_stats``: reduces a ``--kernel-trace --stats`` kernel_stats.csv to
+the stage's kernels (calls, average and total duration).
+
+``traffic``: turns two ``--pmc FETCH_SIZE`` / ``--pmc WRITE_SIZE`` runs of a
+workload, plus the same two counters read for a plain device copy of known
+size, into HBM bytes per dispatch of each kernel.  Each counter is scaled by
+(known copy bytes / what the counter reported for the copy), so systematic
+under- or over-counting of the counters cancels.
+
+Usage:
+  python -m paper_2606_22541_amd.profiling stats <kernel_stats.csv>
+  python -m paper_2606_22541_amd.profiling traffic --workload c1 \\
+      --fetch <counter_collection.csv> --write <counter_collection.csv> \\
+      --copy-fetch <csv> --copy-write <csv> --copy-bytes N --out profiles/traffic.json
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import glob
+import hashlib
+import json
+import os
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCES = {
+    "gemm_gate_up_swiglu": ["csrc/gemm_bf16.hip", "csrc/common.h", "csrc/kernels.h"],
+    "gemm_down": ["csrc/gemm_bf16.hip", "csrc/common.h", "csrc/kernels.h"],
+    "combine": ["csrc/combine.hip", "csrc/common.h", "csrc/kernels.h"],
+    "gather": ["csrc/dispatch.hip", "csrc/common.h", "csrc/kernels.h"],
+}
+# rocprof kernel-name prefixes of the stage's kernels -> bench kernel kinds
+NAME_MAP = (
+    ("void moe::k_gemm_bf16<true>", "gemm_gate_up_swiglu"),
+    ("void moe::k_gemm_bf16<false>", "gemm_down"),
+    ("void moe::k_gemm_fp8<true>", "gemm_gate_up_swiglu_fp8"),
+    ("void moe::k_gemm_fp8<false>", "gemm_down_fp8"),
+    ("moe::k_combine", "combine"),
+    ("moe::k_gather", "gather"),
+    ("moe::k_hist", "hist"),
+    ("moe::k_scan", "scan"),
+    ("moe::k_scatter", "scatter"),
+    ("moe::k_quantize_fp8", "quantize_fp8"),
+)
+COPY_NAMES = ("__amd_rocclr_copyBuffer",)
+
+
+def sources_digest(kind: str) -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES.get(kind, []):
+        with open(os.path.join(PKG, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def kind_of(name: str):
+    for prefix, kind in NAME_MAP:
+        if name.startswith(prefix):
+            return kind
+    return None
+
+
+def _find_csv(path: str, suffix: str) -> str:
+    if os.path.isdir(path):
+        hits = glob.glob(os.path.join(path, "**", "*" + suffix), recursive=True)
+        if not hits:
+            raise FileNotFoundError("no *%s under %s" % (suffix, path))
+        return hits[0]
+    return path
+
+
+def kernel_stats(path: str):
+    rows = list(csv.DictReader(open(_find_csv(path, "kernel_stats.csv"))))
+    out = {}
+    for r in rows:
+        k = kind_of(r["Name"])
+        if k:
+            out[k] = {"calls": int(r["Calls"]), "avg_ms": float(r["AverageNs"]) / 1e6,
+                      "total_ms": float(r["TotalDurationNs"]) / 1e6}
+    return out
+
+
+def counter_per_dispatch(path: str, counter: str):
+    """Mean counter value per dispatch, by kernel kind (copy kernels too)."""
+    rows = list(csv.DictReader(open(_find_csv(path, "counter_collection.csv"))))
+    acc = collections.defaultdict(float)
+    disp = collections.defaultdict(set)
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        name = r["Kernel_Name"]
+        k = kind_of(name) or (name if name in COPY_NAMES else None)
+        if k is None:
+            continue
+        acc[k] += float(r["Counter_Value"])
+        disp[k].add(r["Dispatch_Id"])
+    return {k: acc[k] / len(disp[k]) for k in acc}
+
+
+def traffic(args):
+    fetch = counter_per_dispatch(args.fetch, "FETCH_SIZE")
+    write = counter_per_dispatch(args.write, "WRITE_SIZE")
+    cf = counter_per_dispatch(args.copy_fetch, "FETCH_SIZE")
+    cw = counter_per_dispatch(args.copy_write, "WRITE_SIZE")
+    copy = COPY_NAMES[0]
+    # the largest copy dispatch is the calibration copy
+    f_scale = args.copy_bytes / (cf[copy] * 1024.0)
+    w_scale = args.copy_bytes / (cw[copy] * 1024.0)
+    rec = json.load(open(args.out)) if os.path.exists(args.out) else {}
+    rec.setdefault("kernels", {})
+    rec["calibration"] = {"copy_bytes": args.copy_bytes, "fetch_kib": cf[copy],
+                          "write_kib": cw[copy], "fetch_scale": f_scale, "write_scale": w_scale}
+    for k in sorted(set(fetch) | set(write)):
+        if k == copy:
+            continue
+        fb = fetch.get(k, 0.0) * 1024.0 * f_scale
+        wb = write.get(k, 0.0) * 1024.0 * w_scale
+        rec["kernels"]["%s:%s" % (args.workload, k)] = {
+            "fetch_bytes_per_dispatch": round(fb), "write_bytes_per_dispatch": round(wb),
+            "bytes_per_dispatch": round(fb + wb), "source_sha256": sources_digest(k)}
+    rec.setdefault("commands", [])
+    if args.command:
+        rec["commands"].append(args.command)
+    with open(args.out, "w") as f:
+        json.dump(rec, f, indent=1, sort_keys=True)
+    print(json.dumps(rec, indent=1, sort_keys=True))
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("path")
+    t = sub.add_parser("traffic")
+    t.add_argument("--workload", required=True)
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--copy-fetch", required=True)
+    t.add_argument("--copy-write", required=True)
+    t.add_argument("--copy-bytes", type=int, required=True)
+    t.add_argument("--out", required=True)
+    t.add_argument("--command", default="")
+    a = ap.parse_args(argv)
+    if a.cmd == "stats":
+        print(json.dumps(kernel_stats(a.path), indent=1, sort_keys=True))
+    else:
+        traffic(a)
+
+
+if __name__ == "__main__":
+    main()
