@@ -27,11 +27,19 @@ constexpr int kBN = 256;
 // Sticky error bits.
 constexpr int kErrBadId = 1;
 
+// Groups with at most this many rows ("small": a DeepSeek EP32 share at
+// T=4096 has ~128 rows per expert) take one full-height tile in the bf16
+// small-group GEMM, which streams each weight panel exactly once; larger
+// groups use the 256x256-tile GEMM.
+constexpr int kSmallRows = 192;
+
 // Device-side tables written by the dispatch scan, read by the GEMMs.
 struct GroupTable {
     int32_t *row0;      // [G] first row of the group in its A matrix
     int32_t *rows;      // [G] rows of the group
-    int32_t *mt_base;   // [G+1] prefix of ceil(rows / kBM)
+    int32_t *mt_base;   // [G+1] prefix of ceil(rows / kBM) over all groups
+    int32_t *lt_base;   // [G+1] same, counting only groups with rows > kSmallRows
+    int32_t *st_base;   // [G+1] prefix of 1 per group with 1 <= rows <= kSmallRows
 };
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }

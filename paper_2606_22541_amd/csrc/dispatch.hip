@@ -61,21 +61,24 @@ void k_scan(const int32_t *__restrict__ blk_counts, int32_t nb, int32_t E, int32
         int run = 0;
         for (int i = 0; i < E_loc; ++i) { off[i] = run; run += c[e0 + i]; }
         off[E_loc] = run;
-        // tile table over G = E_loc (+1 shared) groups
-        int mt = 0;
-        for (int i = 0; i < E_loc; ++i) {
-            g.row0[i] = off[i];
-            g.rows[i] = c[e0 + i];
+        // tile tables over G = E_loc (+1 shared) groups
+        int mt = 0, lt = 0, st = 0;
+        const int G = E_loc + (has_shared ? 1 : 0);
+        for (int i = 0; i < G; ++i) {
+            const int rows = (i < E_loc) ? c[e0 + i] : T;
+            g.row0[i] = (i < E_loc) ? off[i] : 0;
+            g.rows[i] = rows;
             g.mt_base[i] = mt;
-            mt += (c[e0 + i] + kBM - 1) / kBM;
+            g.lt_base[i] = lt;
+            g.st_base[i] = st;
+            const int m = (rows + kBM - 1) / kBM;
+            mt += m;
+            if (rows > kSmallRows) lt += m;
+            else if (rows > 0) st += 1;
         }
-        if (has_shared) {
-            g.row0[E_loc] = 0;
-            g.rows[E_loc] = T;
-            g.mt_base[E_loc] = mt;
-            mt += (T + kBM - 1) / kBM;
-        }
-        g.mt_base[E_loc + (has_shared ? 1 : 0)] = mt;
+        g.mt_base[G] = mt;
+        g.lt_base[G] = lt;
+        g.st_base[G] = st;
     }
     __syncthreads();
     for (int i = threadIdx.x; i <= E_loc; i += blockDim.x) offsets[i] = off[i];
@@ -152,8 +155,119 @@ void k_scatter(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E, int3
     }
 }
 
+// ---------------------------------------------------------------------------
+// Fused single-workgroup dispatch for micro-batches of up to
+// kFusedMaxSlots slots (a 4096-token DeepSeek-V3 batch has 32768): the
+// histogram, scan, tile tables and stable scatter of the three kernels above
+// in one launch, so the dispatch costs one launch instead of three.  Wave w
+// owns the contiguous slot range [w * per, (w + 1) * per).
+// ---------------------------------------------------------------------------
+constexpr int kFusedThreads = 1024;
+constexpr int kFusedWaves = kFusedThreads / 64;
+constexpr int kFusedMaxSlots = 65536;
+
+__global__ __launch_bounds__(kFusedThreads)
+void k_dispatch_fused(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E, int32_t e0,
+                      int32_t E_loc, int32_t T, int32_t has_shared, int32_t *__restrict__ counts,
+                      int32_t *__restrict__ offsets, GroupTable g,
+                      int32_t *__restrict__ slot_of_row, int32_t *__restrict__ row_of_slot,
+                      int32_t *__restrict__ err)
+{
+    __shared__ int32_t h[kMaxExperts];
+    __shared__ int32_t wbase[kFusedWaves][kMaxLocalExperts];
+    __shared__ int32_t off[kMaxLocalExperts + 1];
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int per = ((n_slots + kFusedWaves * 64 - 1) / (kFusedWaves * 64)) * 64;
+    const int64_t wstart = (int64_t)wave * per;
+
+    for (int e = threadIdx.x; e < E; e += kFusedThreads) h[e] = 0;
+    for (int i = lane; i < E_loc; i += 64) wbase[wave][i] = 0;
+    __syncthreads();
+    int bad = 0;
+    for (int st = 0; st < per; st += 64) {
+        const int64_t s = wstart + st + lane;
+        if (s >= n_slots) break;
+        const int e = ids[s];
+        if (e >= 0 && e < E) {
+            atomicAdd(&h[e], 1);                       // integer counts: order-free
+            const int i = e - e0;
+            if (i >= 0 && i < E_loc) atomicAdd(&wbase[wave][i], 1);
+        } else if (e != -1) {
+            bad = 1;
+        }
+    }
+    if (bad) atomicOr(err, kErrBadId);
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += kFusedThreads) counts[e] = h[e];
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int i = 0; i < E_loc; ++i) { off[i] = run; run += h[e0 + i]; }
+        off[E_loc] = run;
+        int mt = 0, lt = 0, stt = 0;
+        const int G = E_loc + (has_shared ? 1 : 0);
+        for (int i = 0; i < G; ++i) {
+            const int rows = (i < E_loc) ? h[e0 + i] : T;
+            g.row0[i] = (i < E_loc) ? off[i] : 0;
+            g.rows[i] = rows;
+            g.mt_base[i] = mt;
+            g.lt_base[i] = lt;
+            g.st_base[i] = stt;
+            const int m = (rows + kBM - 1) / kBM;
+            mt += m;
+            if (rows > kSmallRows) lt += m;
+            else if (rows > 0) stt += 1;
+        }
+        g.mt_base[G] = mt;
+        g.lt_base[G] = lt;
+        g.st_base[G] = stt;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i <= E_loc; i += kFusedThreads) offsets[i] = off[i];
+    // exclusive scan of the per-wave counts, seeded with the expert offsets
+    for (int i = threadIdx.x; i < E_loc; i += kFusedThreads) {
+        int run = off[i];
+        for (int w = 0; w < kFusedWaves; ++w) {
+            const int t = wbase[w][i];
+            wbase[w][i] = run;
+            run += t;
+        }
+    }
+    __syncthreads();
+    volatile int32_t *mybase = wbase[wave];
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int st = 0; st < per; st += 64) {
+        const int64_t s = wstart + st + lane;
+        const bool in = s < n_slots;
+        const int e = in ? ids[s] : -1;
+        const int i = e - e0;
+        const bool loc = in && e >= 0 && e < E && i >= 0 && i < E_loc;
+        uint64_t pending = __ballot(loc);
+        int pos = -1;
+        while (pending) {
+            const int leader = __ffsll((unsigned long long)pending) - 1;
+            const int il = __shfl(i, leader);
+            const uint64_t m = __ballot(loc && i == il);
+            const int b = mybase[il];
+            if (loc && i == il) pos = b + __popcll(m & lt_mask);
+            if (lane == leader) mybase[il] = b + __popcll(m);
+            pending &= ~m;
+        }
+        if (in) {
+            row_of_slot[s] = pos;
+            if (pos >= 0) slot_of_row[pos] = (int32_t)s;
+        }
+    }
+}
+
 hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)
 {
+    if (a.n_slots <= kFusedMaxSlots) {
+        hipLaunchKernelGGL(k_dispatch_fused, dim3(1), dim3(kFusedThreads), 0, s, a.ids, a.n_slots,
+                           a.E, a.e0, a.E_loc, a.T, a.has_shared, a.counts, a.offsets, a.groups,
+                           a.slot_of_row, a.row_of_slot, a.err);
+        return hipGetLastError();
+    }
     const int nb = (a.n_slots + kDispatchChunk - 1) / kDispatchChunk;
     if (nb > 0) {
         hipLaunchKernelGGL(k_hist, dim3(nb), dim3(kDispatchThreads), 0, s, a.ids, a.n_slots, a.E,
@@ -169,41 +283,38 @@ hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)
 }
 
 // ---------------------------------------------------------------------------
-// 4. Row gather: one wave per row, each lane moving up to 8 16-byte chunks
-//    per round (all loads issued before the stores).
+// 4. Row gather: one workgroup per row (grid-stride), each thread moving up
+//    to 4 16-byte chunks of the row with all loads issued before the stores.
 // ---------------------------------------------------------------------------
-constexpr int kGatherWaves = 4;
-constexpr int kGatherUnroll = 8;
+constexpr int kGatherThreads = 256;
+constexpr int kGatherUnroll = 4;
 
-__global__ __launch_bounds__(64 * kGatherWaves)
+__global__ __launch_bounds__(kGatherThreads)
 void k_gather(const uint4 *__restrict__ x, const float *__restrict__ xs,
               const int32_t *__restrict__ slot_of_row, const int32_t *__restrict__ n_rows_dev,
               int32_t k, int32_t row_vecs, int32_t n_scales, uint4 *__restrict__ xp,
               float *__restrict__ xps, int32_t scale_ld)
 {
     const int n_rows = *n_rows_dev;
-    const int lane = threadIdx.x & 63;
-    const int gw = blockIdx.x * kGatherWaves + (threadIdx.x >> 6);
-    const int nw = gridDim.x * kGatherWaves;
-    for (int r = gw; r < n_rows; r += nw) {
+    for (int r = blockIdx.x; r < n_rows; r += gridDim.x) {
         const int t = slot_of_row[r] / k;
         const uint4 *src = x + (int64_t)t * row_vecs;
         uint4 *dst = xp + (int64_t)r * row_vecs;
-        for (int c0 = 0; c0 < row_vecs; c0 += 64 * kGatherUnroll) {
+        for (int c0 = 0; c0 < row_vecs; c0 += kGatherThreads * kGatherUnroll) {
             uint4 v[kGatherUnroll];
 #pragma unroll
             for (int u = 0; u < kGatherUnroll; ++u) {
-                const int c = c0 + u * 64 + lane;
+                const int c = c0 + u * kGatherThreads + threadIdx.x;
                 if (c < row_vecs) v[u] = src[c];
             }
 #pragma unroll
             for (int u = 0; u < kGatherUnroll; ++u) {
-                const int c = c0 + u * 64 + lane;
+                const int c = c0 + u * kGatherThreads + threadIdx.x;
                 if (c < row_vecs) dst[c] = v[u];
             }
         }
         if (xs != nullptr)
-            for (int c = lane; c < n_scales; c += 64)
+            for (int c = threadIdx.x; c < n_scales; c += kGatherThreads)
                 xps[(int64_t)c * scale_ld + r] = xs[(int64_t)t * n_scales + c];
     }
 }
@@ -214,10 +325,9 @@ hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_
                               int32_t scale_ld, int32_t max_rows, int num_cus, hipStream_t s)
 {
     if (max_rows <= 0) return hipSuccess;
-    int grid = num_cus * 8;
-    const int need = (max_rows + kGatherWaves - 1) / kGatherWaves;
-    if (grid > need) grid = need;
-    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(64 * kGatherWaves), 0, s, (const uint4 *)x,
+    int grid = num_cus * 16;
+    if (grid > max_rows) grid = max_rows;
+    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kGatherThreads), 0, s, (const uint4 *)x,
                        x_scales, slot_of_row, n_rows_dev, k, row_bytes / 16, n_scales,
                        (uint4 *)x_perm, x_perm_scales, scale_ld);
     return hipGetLastError();

@@ -24,8 +24,11 @@
 //    XCD, and within a group tiles are rastered in bands of 4 row-tiles,
 //    letting one XCD's L2 serve 4 row panels x 8 weight panels at a time.
 //  * SwiGLU mode fuses h = SiLU(gate) * up into the epilogue: the weight
-//    matrix packs gate and up rows in interleaved blocks of 32, so each wave
-//    holds matching gate and up accumulators in the same registers.
+//    matrix packs gate and up rows in interleaved blocks of 16, so every
+//    32-column MFMA block holds matching gate and up columns, paired across
+//    lanes l and l ^ 16;
+//  * for the gate/up product, groups of at most kSmallRows rows are left to
+//    the small-group kernel (large_all = 0).
 #include "kernels.h"
 
 namespace moe {
@@ -99,7 +102,8 @@ void k_gemm_bf16(GemmArgs a)
     const int wm = wave >> 2, wn = wave & 3;            // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
     const int NT = (N + kBN - 1) / kBN;
-    const int total = __builtin_amdgcn_readfirstlane(a.groups.mt_base[a.G] * NT);
+    const int32_t *tbase = a.large_all ? a.groups.mt_base : a.groups.lt_base;
+    const int total = __builtin_amdgcn_readfirstlane(tbase[a.G] * NT);
     const int KT = K / kBK;
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
@@ -115,7 +119,7 @@ void k_gemm_bf16(GemmArgs a)
 
     for (int L = first; L < total; L += P) {
         int g, mt, nt;
-        decode_tile(L, a.groups.mt_base, a.G, NT, g, mt, nt);
+        decode_tile(L, tbase, a.G, NT, g, mt, nt);
         g = __builtin_amdgcn_readfirstlane(g);
         mt = __builtin_amdgcn_readfirstlane(mt);
         nt = __builtin_amdgcn_readfirstlane(nt);
@@ -200,19 +204,25 @@ void k_gemm_bf16(GemmArgs a)
         // 8 (r / 4) + 4 (lane / 32) + r % 4 and column lane % 32.
         bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
         if constexpr (SWIGLU) {
+            // Packed columns interleave gate and up by 16: in each 32-column
+            // block, lanes 0-15 hold gate and lanes 16-31 up of the same 16
+            // h columns; lane l pairs with lane l ^ 16.
             const int f = N / 2;
-            const int f0 = nt * (kBN / 2) + wn * 32 + (lane & 31);
+            const bool gl = (lane & 16) == 0;
 #pragma unroll
-            for (int mb = 0; mb < 4; ++mb)
+            for (int nb = 0; nb < 2; ++nb) {
+                const int hc = (n0 + wn * 64 + nb * 32) / 2 + (lane & 15);
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int lr = wm * 128 + mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
-                    if (lr < rows_valid) {
-                        const float gt = acc[mb][0][r];
-                        const float up = acc[mb][1][r];
-                        C[(int64_t)(row0 + lr) * f + f0] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+                for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const float v = acc[mb][nb][r];
+                        const float up = __shfl_xor(v, 16);
+                        const int lr = wm * 128 + mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
+                        if (gl && lr < rows_valid)
+                            C[(int64_t)(row0 + lr) * f + hc] = f2bf(v / (1.0f + __expf(-v)) * up);
                     }
-                }
+            }
         } else {
             const int c0 = n0 + wn * 64 + (lane & 31);
 #pragma unroll

@@ -54,6 +54,7 @@ struct GemmArgs {
     int32_t shared_group;    // index of the shared group, -1 if none
     GroupTable groups;
     int32_t G;
+    int32_t large_all;       // bf16 256x256 kernel: 1 = every group, 0 = only rows > kSmallRows
 };
 
 // bf16 grouped GEMM.  swiglu = true: B is the packed [gate|up] matrix
@@ -62,6 +63,10 @@ struct GemmArgs {
 // 256-row tiles over all groups (the grid is sized from it).
 hipError_t launch_gemm_bf16(const GemmArgs &a, bool swiglu, int mt_max, int num_cus,
                             hipStream_t s);
+// bf16 grouped GEMM for the groups with 1..kSmallRows rows: one 256-row x
+// 128-column tile per (group, column block); g_max bounds the group count.
+hipError_t launch_gemm_bf16_small(const GemmArgs &a, bool swiglu, int g_max, int num_cus,
+                                  hipStream_t s);
 
 // e4m3 grouped GEMM with 128-block scales (same conventions; the A scales
 // are transposed, [K/128][ld] with ld = lds_rows_routed / lds_rows_shared).
@@ -87,11 +92,15 @@ hipError_t launch_quantize_fp8(const void *x, int32_t n_rows, const int32_t *n_r
                                hipStream_t s);
 
 // Weight packing at create time.
-// Interleaves gate and up rows in blocks of 32: packed row 64*b + i is gate
-// row 32*b + i for i < 32 and up row 32*b + (i - 32) otherwise.  elem_bytes
-// is 2 (bf16) or 1 (e4m3).
+// Interleaves gate and up rows in blocks of `interleave` rows: packed row
+// 2*il*b + i is gate row il*b + i for i < il and up row il*b + (i - il)
+// otherwise.  bf16 uses il = 16 (a 32-column MFMA block then holds matching
+// gate and up columns), fp8 uses il = 32.  elem_bytes is 2 (bf16) or 1 (e4m3).
+constexpr int kInterleaveBf16 = 16;
+constexpr int kInterleaveFp8 = 32;
 hipError_t launch_pack_gate_up(const void *gate, const void *up, void *packed, int32_t n_mats,
-                               int32_t f, int32_t d, int32_t elem_bytes, hipStream_t s);
+                               int32_t f, int32_t d, int32_t elem_bytes, int32_t interleave,
+                               hipStream_t s);
 // Per-32-row scales of the packed matrix from the 128x128 block scales:
 // packed_s[m][p32][kb] = (gate or up)_s[m][(32*b)/128][kb].
 hipError_t launch_pack_gate_up_scales(const float *gs, const float *us, float *packed_s,

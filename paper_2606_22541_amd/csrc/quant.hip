@@ -72,7 +72,7 @@ hipError_t launch_quantize_fp8(const void *x, int32_t n_rows, const int32_t *n_r
 // ---------------------------------------------------------------------------
 __global__ void k_pack_gate_up(const uint4 *__restrict__ gate, const uint4 *__restrict__ up,
                                uint4 *__restrict__ packed, int32_t n_mats, int32_t f,
-                               int32_t row_vecs)
+                               int32_t row_vecs, int32_t il)
 {
     const int64_t total = (int64_t)n_mats * 2 * f * row_vecs;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
@@ -81,19 +81,20 @@ __global__ void k_pack_gate_up(const uint4 *__restrict__ gate, const uint4 *__re
         const int c = (int)(q - prow * row_vecs);
         const int m = (int)(prow / (2 * f));
         const int p = (int)(prow - (int64_t)m * 2 * f);
-        const int b = p >> 6, i = p & 63;
-        const int src_row = b * 32 + (i & 31);
-        const uint4 *src = (i < 32) ? gate : up;
+        const int b = p / (2 * il), i = p % (2 * il);
+        const int src_row = b * il + (i % il);
+        const uint4 *src = (i < il) ? gate : up;
         packed[q] = src[((int64_t)m * f + src_row) * row_vecs + c];
     }
 }
 
 hipError_t launch_pack_gate_up(const void *gate, const void *up, void *packed, int32_t n_mats,
-                               int32_t f, int32_t d, int32_t elem_bytes, hipStream_t s)
+                               int32_t f, int32_t d, int32_t elem_bytes, int32_t interleave,
+                               hipStream_t s)
 {
     const int row_vecs = d * elem_bytes / 16;
     hipLaunchKernelGGL(k_pack_gate_up, dim3(4096), dim3(256), 0, s, (const uint4 *)gate,
-                       (const uint4 *)up, (uint4 *)packed, n_mats, f, row_vecs);
+                       (const uint4 *)up, (uint4 *)packed, n_mats, f, row_vecs, interleave);
     return hipGetLastError();
 }
 

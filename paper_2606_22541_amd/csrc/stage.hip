@@ -22,6 +22,7 @@ namespace {
 struct SlotWs {
     int32_t *blk_counts = nullptr, *counts = nullptr, *offsets = nullptr, *blk_base = nullptr;
     int32_t *g_row0 = nullptr, *g_rows = nullptr, *g_mt_base = nullptr;
+    int32_t *g_lt_base = nullptr, *g_st_base = nullptr;
     int32_t *slot_of_row = nullptr, *row_of_slot = nullptr;
     void *x_perm = nullptr;
     float *x_perm_s = nullptr;
@@ -89,7 +90,7 @@ Sizes sizes_of(const moe_stage_desc *d)
     int64_t b = 0;
     b += align256(s.nb_max * E * 4) + align256(E * 4) + align256((El + 1) * 4);
     b += align256(s.nb_max * El * 4);
-    b += 2 * align256(s.G * 4) + align256((s.G + 1) * 4);
+    b += 2 * align256(s.G * 4) + 3 * align256((s.G + 1) * 4);
     b += align256(cap1 * 4) + align256((s.n_slots_tok > 0 ? s.n_slots_tok : 1) * 4);
     b += align256(cap1 * D * s.eb) + (fp8 ? align256(cap1 * (D / 128) * 4) : 0);
     b += align256(cap1 * F * s.eb) + (fp8 ? align256(cap1 * (F / 128) * 4) : 0);
@@ -257,14 +258,15 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
     // shared expert is group E_loc.
     hipError_t e = hipSuccess;
     const int64_t w1_mat = 2 * F * D * z.eb, w2_mat = D * F * z.eb;
+    const int32_t il = fp8 ? kInterleaveFp8 : kInterleaveBf16;
     e = launch_pack_gate_up(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)F, (int32_t)D,
-                            (int32_t)z.eb, st->own);
+                            (int32_t)z.eb, il, st->own);
     if (e == hipSuccess)
         e = hipMemcpyAsync(st->w2, w->w_down, (size_t)(El * w2_mat), hipMemcpyDeviceToDevice,
                            st->own);
     if (e == hipSuccess && desc->has_shared_expert) {
         e = launch_pack_gate_up(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
-                                (int32_t)F, (int32_t)D, (int32_t)z.eb, st->own);
+                                (int32_t)F, (int32_t)D, (int32_t)z.eb, il, st->own);
         if (e == hipSuccess)
             e = hipMemcpyAsync((char *)st->w2 + El * w2_mat, w->sh_down, (size_t)w2_mat,
                                hipMemcpyDeviceToDevice, st->own);
@@ -297,7 +299,8 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
         ok = alloc(st, &sl.blk_counts, z.nb_max * E * 4) && alloc(st, &sl.counts, E * 4) &&
              alloc(st, &sl.offsets, (El + 1) * 4) && alloc(st, &sl.blk_base, z.nb_max * El * 4) &&
              alloc(st, &sl.g_row0, z.G * 4) && alloc(st, &sl.g_rows, z.G * 4) &&
-             alloc(st, &sl.g_mt_base, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
+             alloc(st, &sl.g_mt_base, (z.G + 1) * 4) && alloc(st, &sl.g_lt_base, (z.G + 1) * 4) &&
+             alloc(st, &sl.g_st_base, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
              alloc(st, &sl.row_of_slot, (z.n_slots_tok > 0 ? z.n_slots_tok : 1) * 4) &&
              alloc(st, &sl.x_perm, cap1 * D * z.eb) && alloc(st, &sl.h, cap1 * F * z.eb) &&
              alloc(st, &sl.y_perm, cap1 * D * 2);
@@ -366,7 +369,7 @@ moe_status moe_dispatch(moe_stage *st, int32_t slot, const moe_microbatch *mb, v
     a.counts = sl.counts;
     a.offsets = sl.offsets;
     a.blk_base = sl.blk_base;
-    a.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base};
+    a.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base};
     a.slot_of_row = sl.slot_of_row;
     a.row_of_slot = sl.row_of_slot;
     a.err = st->err;
@@ -417,7 +420,7 @@ moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
     g1.N = 2 * d.d_ff;
     g1.K = d.d_model;
     g1.shared_group = d.has_shared_expert ? d.n_local_experts : -1;
-    g1.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base};
+    g1.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base};
     g1.G = (int32_t)st->sz.G;
 
     GemmArgs g2 = g1;
@@ -435,10 +438,17 @@ moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
     const int mt = mt_max > 0x7fffffff ? 0x7fffffff : (int)mt_max;
     const int32_t cap = (int32_t)st->sz.cap, tmax = d.max_tokens;
     hipError_t e;
+    // bf16: groups of at most kSmallRows rows run in the small-group kernel,
+    // the others in the 256x256-tile kernel (either may find no tiles).
+    const int gmax = (int)st->sz.G;
     {
         ProfScope ps(st, 2, s);
-        e = fp8 ? launch_gemm_fp8(g1, true, mt, st->num_cus, cap, tmax, s)
-                : launch_gemm_bf16(g1, true, mt, st->num_cus, s);
+        if (fp8) {
+            e = launch_gemm_fp8(g1, true, mt, st->num_cus, cap, tmax, s);
+        } else {
+            e = launch_gemm_bf16_small(g1, true, gmax, st->num_cus, s);
+            if (e == hipSuccess) e = launch_gemm_bf16(g1, true, mt, st->num_cus, s);
+        }
     }
     if (e == hipSuccess && fp8) {
         // quantise h per row and 128 channels (scales transposed for the down GEMM)
@@ -451,8 +461,14 @@ moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
     }
     if (e == hipSuccess) {
         ProfScope ps(st, 3, s);
-        e = fp8 ? launch_gemm_fp8(g2, false, mt, st->num_cus, cap, tmax, s)
-                : launch_gemm_bf16(g2, false, mt, st->num_cus, s);
+        if (fp8) {
+            e = launch_gemm_fp8(g2, false, mt, st->num_cus, cap, tmax, s);
+        } else {
+            // the down product (K = f) keeps 256x256 tiles for every group:
+            // at ~130 rows its 28 column tiles per expert already fill the GPU
+            g2.large_all = 1;
+            e = launch_gemm_bf16(g2, false, mt, st->num_cus, s);
+        }
     }
     if (e == hipErrorNotSupported) return MOE_EUNSUPPORTED;
     if (e != hipSuccess) return MOE_EHIP;
