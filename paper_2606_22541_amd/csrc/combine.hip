@@ -9,9 +9,12 @@
 
 namespace moe {
 
-// One workgroup per token (grid-stride).  The token's k rows and weights
-// are wave-uniform loads; each thread owns up to kUnroll 16-byte channel
-// chunks c = tid + 256 u and issues all loads of a slot before using them.
+// One workgroup per token (grid-stride).  The token's k row indices and
+// weights are uniform loads; thread tid owns the 16-byte channel chunks
+// c = c0 + 256 u + tid.  Loads use indices clamped into the row so that they
+// are unconditional (a guarded load would be issued and waited for one at a
+// time); only the stores are guarded.  A scheduling barrier after each batch
+// of loads keeps the compiler from interleaving them with the conversions.
 constexpr int kCombineThreads = 256;
 constexpr int kUnroll = 4;
 
@@ -34,20 +37,35 @@ void k_combine(const uint4 *__restrict__ y, const uint4 *__restrict__ ysh,
         uint4 *orow = out + (int64_t)t * vecs;
         const uint4 *shrow = ysh ? ysh + (int64_t)t * vecs : nullptr;
         for (int c0 = 0; c0 < vecs; c0 += kCombineThreads * kUnroll) {
-            float acc[kUnroll][8];
+            int cc[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int c = c0 + u * kCombineThreads + threadIdx.x;
-                if (accumulate && c < vecs) {
-                    const uint4 o = orow[c];
-                    const bf16 *ob = (const bf16 *)&o;
+            for (int u = 0; u < kUnroll; ++u)
+                cc[u] = min(c0 + u * kCombineThreads + (int)threadIdx.x, vecs - 1);
+            float acc[kUnroll][8];
+            if (accumulate) {
+                uint4 o[kUnroll];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) o[u] = orow[cc[u]];
+                __builtin_amdgcn_sched_barrier(0);   // all loads issued first
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    const bf16 *ob = (const bf16 *)&o[u];
 #pragma unroll
                     for (int i = 0; i < 8; ++i) acc[u][i] = bf2f(ob[i]);
-                } else {
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
                     for (int i = 0; i < 8; ++i) acc[u][i] = 0.0f;
-                }
-                if (shrow && c < vecs) acc_row(acc[u], shrow[c], 1.0f);
+            }
+            if (shrow) {
+                uint4 v[kUnroll];
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) v[u] = shrow[cc[u]];
+                __builtin_amdgcn_sched_barrier(0);   // all loads issued first
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) acc_row(acc[u], v[u], 1.0f);
             }
             for (int j = 0; j < k; ++j) {                      // j ascending
                 const int r = row_of_slot[(int64_t)t * k + j];
@@ -56,10 +74,8 @@ void k_combine(const uint4 *__restrict__ y, const uint4 *__restrict__ ysh,
                 const uint4 *yrow = y + (int64_t)r * vecs;
                 uint4 v[kUnroll];
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    const int c = c0 + u * kCombineThreads + threadIdx.x;
-                    v[u] = c < vecs ? yrow[c] : make_uint4(0, 0, 0, 0);
-                }
+                for (int u = 0; u < kUnroll; ++u) v[u] = yrow[cc[u]];
+                __builtin_amdgcn_sched_barrier(0);   // all loads issued first
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) acc_row(acc[u], v[u], wj);
             }

@@ -14,8 +14,39 @@
 
 namespace moe {
 
+constexpr int kWaves = kDispatchThreads / 64;
+constexpr int kPerWave = kDispatchChunk / kWaves;     // slots per wave
+constexpr int kSteps = kPerWave / 64;                 // 64-slot steps per wave
+
+// Exclusive prefix sum of one value per thread over the workgroup; *total
+// receives the sum of all values.  Every thread of the workgroup must call it.
+__device__ int block_excl_scan(int v, int32_t *wsum, int &total)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) wsum[wave] = x;
+    __syncthreads();
+    int pre = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        const int t = wsum[w];
+        if (w < wave) pre += t;
+        tot += t;
+    }
+    __syncthreads();
+    total = tot;
+    return pre + x - v;
+}
+
 // ---------------------------------------------------------------------------
-// 1. Histogram over all experts, one row of counts per workgroup.
+// 1. Histogram over all experts, one row of counts per workgroup of
+//    kDispatchChunk slots.  Loads use clamped indices so that each thread
+//    issues all of its loads before the first use.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kDispatchThreads)
 void k_hist(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E,
@@ -23,272 +54,204 @@ void k_hist(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E,
 {
     __shared__ int32_t h[kMaxExperts];
     for (int e = threadIdx.x; e < E; e += kDispatchThreads) h[e] = 0;
+    const int64_t base = (int64_t)blockIdx.x * kDispatchChunk + threadIdx.x;
+    constexpr int kPer = kDispatchChunk / kDispatchThreads;
+    int v[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int64_t sl = base + (int64_t)j * kDispatchThreads;
+        v[j] = ids[sl < n_slots ? sl : n_slots - 1];
+    }
     __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * kDispatchChunk;
     int bad = 0;
-    for (int i = threadIdx.x; i < kDispatchChunk; i += kDispatchThreads) {
-        int64_t s = base + i;
-        if (s >= n_slots) break;
-        int e = ids[s];
-        if (e >= 0 && e < E) atomicAdd(&h[e], 1);       // integer counts: order-free
-        else if (e != -1) bad = 1;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        if (base + (int64_t)j * kDispatchThreads >= n_slots) continue;
+        if (v[j] >= 0 && v[j] < E) atomicAdd(&h[v[j]], 1);   // integer counts: order-free
+        else if (v[j] != -1) bad = 1;
     }
     if (bad) atomicOr(err, kErrBadId);
     __syncthreads();
-    for (int e = threadIdx.x; e < E; e += kDispatchThreads)
-        blk_counts[(int64_t)blockIdx.x * E + e] = h[e];
+    for (int x = threadIdx.x; x < E; x += kDispatchThreads)
+        blk_counts[(int64_t)blockIdx.x * E + x] = h[x];
 }
 
 // ---------------------------------------------------------------------------
-// 2. Scan (single workgroup): global counts, local offsets, per-workgroup
-//    bases, and the grouped-GEMM tile table.  Nothing returns to the host.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024)
-void k_scan(const int32_t *__restrict__ blk_counts, int32_t nb, int32_t E, int32_t e0,
-            int32_t E_loc, int32_t T, int32_t has_shared, int32_t *__restrict__ counts,
-            int32_t *__restrict__ offsets, int32_t *__restrict__ blk_base, GroupTable g)
-{
-    __shared__ int32_t c[kMaxExperts];
-    __shared__ int32_t off[kMaxLocalExperts + 1];
-    for (int e = threadIdx.x; e < E; e += blockDim.x) {
-        int acc = 0;
-        for (int b = 0; b < nb; ++b) acc += blk_counts[(int64_t)b * E + e];
-        c[e] = acc;
-        counts[e] = acc;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int run = 0;
-        for (int i = 0; i < E_loc; ++i) { off[i] = run; run += c[e0 + i]; }
-        off[E_loc] = run;
-        // tile tables over G = E_loc (+1 shared) groups
-        int mt = 0, lt = 0, st = 0;
-        const int G = E_loc + (has_shared ? 1 : 0);
-        for (int i = 0; i < G; ++i) {
-            const int rows = (i < E_loc) ? c[e0 + i] : T;
-            g.row0[i] = (i < E_loc) ? off[i] : 0;
-            g.rows[i] = rows;
-            g.mt_base[i] = mt;
-            g.lt_base[i] = lt;
-            g.st_base[i] = st;
-            const int m = (rows + kBM - 1) / kBM;
-            mt += m;
-            if (rows > kSmallRows) lt += m;
-            else if (rows > 0) st += 1;
-        }
-        g.mt_base[G] = mt;
-        g.lt_base[G] = lt;
-        g.st_base[G] = st;
-    }
-    __syncthreads();
-    for (int i = threadIdx.x; i <= E_loc; i += blockDim.x) offsets[i] = off[i];
-    for (int i = threadIdx.x; i < E_loc; i += blockDim.x) {
-        int run = off[i];
-        for (int b = 0; b < nb; ++b) {
-            blk_base[(int64_t)b * E_loc + i] = run;
-            run += blk_counts[(int64_t)b * E + e0 + i];
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// 3. Stable scatter.  Wave w of workgroup b owns slots
-//    [b*chunk + w*chunk/4, b*chunk + (w+1)*chunk/4) and walks them in 64-slot
-//    steps; within a step, lanes holding the same expert are ranked by lane
-//    order with a ballot.
+// 2. Placement.  Workgroup b owns the same kDispatchChunk slots as histogram
+//    workgroup b; wave w owns slots [b*chunk + w*chunk/4, b*chunk +
+//    (w+1)*chunk/4) and walks them in 64-slot steps.  Every workgroup reads
+//    the local-expert columns of the histogram rows to get the expert totals
+//    and the counts of the workgroups before it, so no single-workgroup scan
+//    sits between the two kernels.  Workgroup b also writes the global counts
+//    of experts b, b + grid, ...; workgroup 0 writes the offsets and the
+//    grouped-GEMM tile tables.  Within a step, lanes holding the same expert
+//    are ranked by lane order with a ballot.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kDispatchThreads)
-void k_scatter(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E, int32_t e0,
-               int32_t E_loc, const int32_t *__restrict__ blk_base,
-               int32_t *__restrict__ slot_of_row, int32_t *__restrict__ row_of_slot)
+void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, int32_t E,
+             int32_t e0, int32_t E_loc, int32_t T, int32_t has_shared,
+             const int32_t *__restrict__ blk_counts, int32_t *__restrict__ counts,
+             int32_t *__restrict__ offsets, GroupTable g, int32_t *__restrict__ slot_of_row,
+             int32_t *__restrict__ row_of_slot)
 {
-    constexpr int kWaves = kDispatchThreads / 64;
-    constexpr int kPerWave = kDispatchChunk / kWaves;
+    __shared__ int32_t tot[kMaxLocalExperts], pre[kMaxLocalExperts];
     __shared__ int32_t wbase[kWaves][kMaxLocalExperts];
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int64_t wstart = (int64_t)blockIdx.x * kDispatchChunk + (int64_t)wave * kPerWave;
+    __shared__ int32_t cnt_my[kMaxExperts];
+    __shared__ int32_t wsum[kWaves];
+    const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int64_t wstart = (int64_t)b * kDispatchChunk + (int64_t)wave * kPerWave + lane;
 
-    for (int i = lane; i < E_loc; i += 64) wbase[wave][i] = 0;
+    // local expert index of each slot this lane owns (-1: not local / none)
+    int li[kSteps];
+    if (n_slots > 0) {
+        int v[kSteps];
+#pragma unroll
+        for (int j = 0; j < kSteps; ++j) {
+            const int64_t sl = wstart + j * 64;
+            v[j] = ids[sl < n_slots ? sl : n_slots - 1];
+        }
+#pragma unroll
+        for (int j = 0; j < kSteps; ++j) {
+            const int i = v[j] - e0;
+            li[j] = (wstart + j * 64 < n_slots && v[j] >= 0 && v[j] < E && i >= 0 && i < E_loc)
+                        ? i : -1;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kSteps; ++j) li[j] = -1;
+    }
+    const int n_my = b < E ? (E - 1 - b) / (int)gridDim.x + 1 : 0;
+    for (int i = tid; i < E_loc; i += kDispatchThreads) {
+        tot[i] = 0;
+        pre[i] = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) wbase[w][i] = 0;
+    }
+    for (int q = tid; q < n_my; q += kDispatchThreads) cnt_my[q] = 0;
     __syncthreads();
-    // per-wave local counts
-    for (int st = 0; st < kPerWave; st += 64) {
-        int64_t s = wstart + st + lane;
-        int e = (s < n_slots) ? ids[s] : -1;
-        int i = e - e0;
-        if (e >= 0 && e < E && i >= 0 && i < E_loc) atomicAdd(&wbase[wave][i], 1);
+
+    // expert totals and the part of them in earlier workgroups
+    {
+        const int tpe = E_loc < kDispatchThreads ? kDispatchThreads / E_loc : 1;
+        const int i = tid / tpe, sub = tid - i * tpe;
+        if (i < E_loc) {
+            int t = 0, p = 0;
+            for (int bb = sub; bb < nb_hist; bb += tpe) {
+                const int c = blk_counts[(int64_t)bb * E + e0 + i];
+                t += c;
+                if (bb < b) p += c;
+            }
+            atomicAdd(&tot[i], t);
+            atomicAdd(&pre[i], p);
+        }
+    }
+    // per-wave counts of this workgroup's slots
+#pragma unroll
+    for (int j = 0; j < kSteps; ++j)
+        if (li[j] >= 0) atomicAdd(&wbase[wave][li[j]], 1);
+    // global counts of experts b, b + grid, ...
+    for (int it = tid; it < n_my * nb_hist; it += kDispatchThreads) {
+        const int q = it / nb_hist, bb = it - q * nb_hist;
+        atomicAdd(&cnt_my[q], blk_counts[(int64_t)bb * E + b + q * (int)gridDim.x]);
     }
     __syncthreads();
-    // exclusive scan over waves, seeded with this workgroup's base
-    for (int i = threadIdx.x; i < E_loc; i += kDispatchThreads) {
-        int run = blk_base[(int64_t)blockIdx.x * E_loc + i];
+    for (int q = tid; q < n_my; q += kDispatchThreads) counts[b + q * (int)gridDim.x] = cnt_my[q];
+
+    // offsets (E_loc <= 256: one local expert per thread) and wave bases
+    int total = 0;
+    const int off_i = block_excl_scan(tid < E_loc ? tot[tid] : 0, wsum, total);
+    if (tid < E_loc) {
+        int run = off_i + pre[tid];
+#pragma unroll
         for (int w = 0; w < kWaves; ++w) {
-            int t = wbase[w][i];
-            wbase[w][i] = run;
+            const int t = wbase[w][tid];
+            wbase[w][tid] = run;
             run += t;
         }
     }
-    __syncthreads();
-    volatile int32_t *mybase = wbase[wave];
-    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    for (int st = 0; st < kPerWave; st += 64) {
-        int64_t s = wstart + st + lane;
-        bool in = s < n_slots;
-        int e = in ? ids[s] : -1;
-        int i = e - e0;
-        bool loc = in && e >= 0 && e < E && i >= 0 && i < E_loc;
-        uint64_t pending = __ballot(loc);
-        int pos = -1;
-        while (pending) {
-            int leader = __ffsll((unsigned long long)pending) - 1;
-            int il = __shfl(i, leader);
-            uint64_t m = __ballot(loc && i == il);
-            int b = mybase[il];
-            if (loc && i == il) pos = b + __popcll(m & lt_mask);
-            if (lane == leader) mybase[il] = b + __popcll(m);
-            pending &= ~m;
-        }
-        if (in) {
-            row_of_slot[s] = pos;
-            if (pos >= 0) slot_of_row[pos] = (int32_t)s;
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Fused single-workgroup dispatch for micro-batches of up to
-// kFusedMaxSlots slots (a 4096-token DeepSeek-V3 batch has 32768): the
-// histogram, scan, tile tables and stable scatter of the three kernels above
-// in one launch, so the dispatch costs one launch instead of three.  Wave w
-// owns the contiguous slot range [w * per, (w + 1) * per).
-// ---------------------------------------------------------------------------
-constexpr int kFusedThreads = 1024;
-constexpr int kFusedWaves = kFusedThreads / 64;
-constexpr int kFusedMaxSlots = 65536;
-
-__global__ __launch_bounds__(kFusedThreads)
-void k_dispatch_fused(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E, int32_t e0,
-                      int32_t E_loc, int32_t T, int32_t has_shared, int32_t *__restrict__ counts,
-                      int32_t *__restrict__ offsets, GroupTable g,
-                      int32_t *__restrict__ slot_of_row, int32_t *__restrict__ row_of_slot,
-                      int32_t *__restrict__ err)
-{
-    __shared__ int32_t h[kMaxExperts];
-    __shared__ int32_t wbase[kFusedWaves][kMaxLocalExperts];
-    __shared__ int32_t off[kMaxLocalExperts + 1];
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int per = ((n_slots + kFusedWaves * 64 - 1) / (kFusedWaves * 64)) * 64;
-    const int64_t wstart = (int64_t)wave * per;
-
-    for (int e = threadIdx.x; e < E; e += kFusedThreads) h[e] = 0;
-    for (int i = lane; i < E_loc; i += 64) wbase[wave][i] = 0;
-    __syncthreads();
-    int bad = 0;
-    for (int st = 0; st < per; st += 64) {
-        const int64_t s = wstart + st + lane;
-        if (s >= n_slots) break;
-        const int e = ids[s];
-        if (e >= 0 && e < E) {
-            atomicAdd(&h[e], 1);                       // integer counts: order-free
-            const int i = e - e0;
-            if (i >= 0 && i < E_loc) atomicAdd(&wbase[wave][i], 1);
-        } else if (e != -1) {
-            bad = 1;
-        }
-    }
-    if (bad) atomicOr(err, kErrBadId);
-    __syncthreads();
-    for (int e = threadIdx.x; e < E; e += kFusedThreads) counts[e] = h[e];
-    if (threadIdx.x == 0) {
-        int run = 0;
-        for (int i = 0; i < E_loc; ++i) { off[i] = run; run += h[e0 + i]; }
-        off[E_loc] = run;
-        int mt = 0, lt = 0, stt = 0;
+    if (b == 0) {
+        if (tid < E_loc) offsets[tid] = off_i;
+        if (tid == 0) offsets[E_loc] = total;
+        // tile tables over G = E_loc (+1 shared) groups, in chunks of 256
         const int G = E_loc + (has_shared ? 1 : 0);
-        for (int i = 0; i < G; ++i) {
-            const int rows = (i < E_loc) ? h[e0 + i] : T;
-            g.row0[i] = (i < E_loc) ? off[i] : 0;
-            g.rows[i] = rows;
-            g.mt_base[i] = mt;
-            g.lt_base[i] = lt;
-            g.st_base[i] = stt;
+        int c_mt = 0, c_lt = 0, c_st = 0;
+        for (int c0 = 0; c0 < G; c0 += kDispatchThreads) {
+            const int i = c0 + tid;
+            const int rows = i < E_loc ? tot[i] : (i < G ? T : 0);
             const int m = (rows + kBM - 1) / kBM;
-            mt += m;
-            if (rows > kSmallRows) lt += m;
-            else if (rows > 0) stt += 1;
+            const int lt = rows > kSmallRows ? m : 0;
+            const int sm = (rows > 0 && rows <= kSmallRows) ? 1 : 0;
+            int t_mt, t_lt, t_st;
+            const int p_mt = block_excl_scan(m, wsum, t_mt);
+            const int p_lt = block_excl_scan(lt, wsum, t_lt);
+            const int p_st = block_excl_scan(sm, wsum, t_st);
+            if (i < G) {
+                g.row0[i] = i < E_loc ? off_i : 0;
+                g.rows[i] = rows;
+                g.mt_base[i] = c_mt + p_mt;
+                g.lt_base[i] = c_lt + p_lt;
+                g.st_base[i] = c_st + p_st;
+            }
+            c_mt += t_mt;
+            c_lt += t_lt;
+            c_st += t_st;
         }
-        g.mt_base[G] = mt;
-        g.lt_base[G] = lt;
-        g.st_base[G] = stt;
+        if (tid == 0) {
+            g.mt_base[G] = c_mt;
+            g.lt_base[G] = c_lt;
+            g.st_base[G] = c_st;
+        }
     }
     __syncthreads();
-    for (int i = threadIdx.x; i <= E_loc; i += kFusedThreads) offsets[i] = off[i];
-    // exclusive scan of the per-wave counts, seeded with the expert offsets
-    for (int i = threadIdx.x; i < E_loc; i += kFusedThreads) {
-        int run = off[i];
-        for (int w = 0; w < kFusedWaves; ++w) {
-            const int t = wbase[w][i];
-            wbase[w][i] = run;
-            run += t;
-        }
-    }
-    __syncthreads();
+
     volatile int32_t *mybase = wbase[wave];
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    for (int st = 0; st < per; st += 64) {
-        const int64_t s = wstart + st + lane;
-        const bool in = s < n_slots;
-        const int e = in ? ids[s] : -1;
-        const int i = e - e0;
-        const bool loc = in && e >= 0 && e < E && i >= 0 && i < E_loc;
+#pragma unroll
+    for (int j = 0; j < kSteps; ++j) {
+        const int64_t sl = wstart + j * 64;
+        const int i = li[j];
+        const bool loc = i >= 0;
         uint64_t pending = __ballot(loc);
         int pos = -1;
         while (pending) {
             const int leader = __ffsll((unsigned long long)pending) - 1;
             const int il = __shfl(i, leader);
             const uint64_t m = __ballot(loc && i == il);
-            const int b = mybase[il];
-            if (loc && i == il) pos = b + __popcll(m & lt_mask);
-            if (lane == leader) mybase[il] = b + __popcll(m);
+            const int bse = mybase[il];
+            if (loc && i == il) pos = bse + __popcll(m & lt_mask);
+            if (lane == leader) mybase[il] = bse + __popcll(m);
             pending &= ~m;
         }
-        if (in) {
-            row_of_slot[s] = pos;
-            if (pos >= 0) slot_of_row[pos] = (int32_t)s;
+        if (sl < n_slots) {
+            row_of_slot[sl] = pos;
+            if (pos >= 0) slot_of_row[pos] = (int32_t)sl;
         }
     }
 }
 
 hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)
 {
-    if (a.n_slots <= kFusedMaxSlots) {
-        hipLaunchKernelGGL(k_dispatch_fused, dim3(1), dim3(kFusedThreads), 0, s, a.ids, a.n_slots,
-                           a.E, a.e0, a.E_loc, a.T, a.has_shared, a.counts, a.offsets, a.groups,
-                           a.slot_of_row, a.row_of_slot, a.err);
-        return hipGetLastError();
-    }
     const int nb = (a.n_slots + kDispatchChunk - 1) / kDispatchChunk;
     if (nb > 0) {
         hipLaunchKernelGGL(k_hist, dim3(nb), dim3(kDispatchThreads), 0, s, a.ids, a.n_slots, a.E,
                            a.blk_counts, a.err);
     }
-    hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, a.blk_counts, nb, a.E, a.e0, a.E_loc,
-                       a.T, a.has_shared, a.counts, a.offsets, a.blk_base, a.groups);
-    if (nb > 0) {
-        hipLaunchKernelGGL(k_scatter, dim3(nb), dim3(kDispatchThreads), 0, s, a.ids, a.n_slots,
-                           a.E, a.e0, a.E_loc, a.blk_base, a.slot_of_row, a.row_of_slot);
-    }
+    hipLaunchKernelGGL(k_place, dim3(nb > 0 ? nb : 1), dim3(kDispatchThreads), 0, s, a.ids,
+                       a.n_slots, nb, a.E, a.e0, a.E_loc, a.T, a.has_shared, a.blk_counts,
+                       a.counts, a.offsets, a.groups, a.slot_of_row, a.row_of_slot);
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// 4. Row gather: one workgroup per row (grid-stride), each thread moving up
-//    to 4 16-byte chunks of the row with all loads issued before the stores.
+// 4. Row gather: one workgroup per row (grid-stride).  Thread tid moves the
+//    16-byte chunks c0 + 256 u + tid, u < U.  Chunk indices are clamped into
+//    the row rather than guarded, so that all U loads are issued before the
+//    first store; a clamped lane rewrites the row's last chunk with the same
+//    value, which is harmless for a pure copy.
 // ---------------------------------------------------------------------------
 constexpr int kGatherThreads = 256;
-constexpr int kGatherUnroll = 4;
 
+template <int U>
 __global__ __launch_bounds__(kGatherThreads)
 void k_gather(const uint4 *__restrict__ x, const float *__restrict__ xs,
               const int32_t *__restrict__ slot_of_row, const int32_t *__restrict__ n_rows_dev,
@@ -300,18 +263,16 @@ void k_gather(const uint4 *__restrict__ x, const float *__restrict__ xs,
         const int t = slot_of_row[r] / k;
         const uint4 *src = x + (int64_t)t * row_vecs;
         uint4 *dst = xp + (int64_t)r * row_vecs;
-        for (int c0 = 0; c0 < row_vecs; c0 += kGatherThreads * kGatherUnroll) {
-            uint4 v[kGatherUnroll];
+        for (int c0 = 0; c0 < row_vecs; c0 += kGatherThreads * U) {
+            int cc[U];
+            uint4 v[U];
 #pragma unroll
-            for (int u = 0; u < kGatherUnroll; ++u) {
-                const int c = c0 + u * kGatherThreads + threadIdx.x;
-                if (c < row_vecs) v[u] = src[c];
+            for (int u = 0; u < U; ++u) {
+                cc[u] = min(c0 + u * kGatherThreads + (int)threadIdx.x, row_vecs - 1);
+                v[u] = src[cc[u]];
             }
 #pragma unroll
-            for (int u = 0; u < kGatherUnroll; ++u) {
-                const int c = c0 + u * kGatherThreads + threadIdx.x;
-                if (c < row_vecs) dst[c] = v[u];
-            }
+            for (int u = 0; u < U; ++u) dst[cc[u]] = v[u];
         }
         if (xs != nullptr)
             for (int c = threadIdx.x; c < n_scales; c += kGatherThreads)
@@ -327,9 +288,13 @@ hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_
     if (max_rows <= 0) return hipSuccess;
     int grid = num_cus * 16;
     if (grid > max_rows) grid = max_rows;
-    hipLaunchKernelGGL(k_gather, dim3(grid), dim3(kGatherThreads), 0, s, (const uint4 *)x,
-                       x_scales, slot_of_row, n_rows_dev, k, row_bytes / 16, n_scales,
-                       (uint4 *)x_perm, x_perm_scales, scale_ld);
+    const int row_vecs = row_bytes / 16;
+    auto kern = row_vecs > 2 * kGatherThreads ? k_gather<4>
+              : row_vecs > kGatherThreads     ? k_gather<2>
+                                              : k_gather<1>;
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kGatherThreads), 0, s, (const uint4 *)x, x_scales,
+                       slot_of_row, n_rows_dev, k, row_vecs, n_scales, (uint4 *)x_perm,
+                       x_perm_scales, scale_ld);
     return hipGetLastError();
 }
 

@@ -3,21 +3,26 @@
 // With few rows per expert the grouped GEMM is bound by streaming the
 // experts' weights from HBM (at T=4096 of a DeepSeek-V3 EP32 share each of
 // the 8 local experts sees ~130 rows and ~88 MB of weights).  The design
-// aims at reading every weight byte once, from all CUs at once:
+// reads every weight byte once, from all CUs at once, and keeps LDS traffic
+// low enough that it does not hold the weight stream back:
 //  * one tile = all rows of a group (up to 192) x 128 weight columns, so
 //    each weight panel is read exactly once and there are E_loc x N/128
 //    tiles (256 at T=4096) -- enough for every CU;
-//  * four wave64s each own 32 weight columns and all row blocks; MFMAs and
-//    row fills are skipped for 32-row blocks past the group's end;
-//  * a K step (64 wide) is only ~20 MFMAs per wave, so both operands are
-//    fetched three steps ahead through 4-deep direct-to-LDS rings (token
-//    rows: 4 x 24 KB, weights: 4 x 16 KB); the K loop is unrolled by 4 so
-//    every ring index is a compile-time constant and each buffer is its own
-//    LDS object, which lets the compiler see that in-flight fills never
-//    alias the buffer being read; the wait at each step is computed exactly
-//    from the loads this wave issued after the step's own;
-//  * SwiGLU: packed gate/up columns interleave by 16, so a wave's 32
-//    columns are 16 gate and 16 up columns of the same h columns, paired
+//  * the four wave64s form a 2 x 2 grid: wave (kh, ch) owns weight columns
+//    [64 ch, 64 ch + 64) and the K half [32 kh, 32 kh + 32) of every 64-wide
+//    K step, for all row blocks; the two K halves are summed through LDS
+//    once per tile;
+//  * weights go straight from HBM into a 4-deep register ring (each wave
+//    loads only its own columns and K half: four 1 KB fragments per step,
+//    each a contiguous load thanks to the fragment-order weight layout), so
+//    LDS carries only the token rows: a direct-to-LDS 4-deep ring
+//    (4 x 24 KB) read as MFMA fragments, two per row block per step;
+//  * the K loop is unrolled by 4 so every ring index is a compile-time
+//    constant, and every step issues the same loads (steps past K re-read
+//    the last one), so the wait at each step is a constant: the loads of
+//    the two steps issued after it;
+//  * SwiGLU: packed gate/up columns interleave by 16, so each 32-column
+//    block is 16 gate and 16 up columns of the same h columns, paired
 //    across lanes l and l ^ 16.
 #include "kernels.h"
 
@@ -49,24 +54,10 @@ __device__ __forceinline__ void rows8_to_lds(__amdgpu_buffer_rsrc_t r, bf16 *til
                                              soff, 0, 0);
 }
 
-// s_waitcnt vmcnt(n) for a wave-uniform n in [0, 31] (larger n: 31).
-__device__ __forceinline__ void wait_vmcnt(int n)
+__device__ __forceinline__ bf16x8 load_b128(__amdgpu_buffer_rsrc_t r, int voff, int soff)
 {
-    constexpr int E = (7 << 4) | (15 << 8);          // expcnt, lgkmcnt: no wait
-#define MOE_WAIT_CASE(v) case v: __builtin_amdgcn_s_waitcnt((v) | E); break;
-    switch (n) {
-        MOE_WAIT_CASE(0) MOE_WAIT_CASE(1) MOE_WAIT_CASE(2) MOE_WAIT_CASE(3)
-        MOE_WAIT_CASE(4) MOE_WAIT_CASE(5) MOE_WAIT_CASE(6) MOE_WAIT_CASE(7)
-        MOE_WAIT_CASE(8) MOE_WAIT_CASE(9) MOE_WAIT_CASE(10) MOE_WAIT_CASE(11)
-        MOE_WAIT_CASE(12) MOE_WAIT_CASE(13) MOE_WAIT_CASE(14) MOE_WAIT_CASE(15)
-    default:
-        if (n >= 31) __builtin_amdgcn_s_waitcnt((31 & 15) | ((31 >> 4) << 14) | E);
-        else if (n >= 24) __builtin_amdgcn_s_waitcnt((24 & 15) | ((24 >> 4) << 14) | E);
-        else if (n >= 20) __builtin_amdgcn_s_waitcnt((20 & 15) | ((20 >> 4) << 14) | E);
-        else __builtin_amdgcn_s_waitcnt((16 & 15) | ((16 >> 4) << 14) | E);
-        break;
-    }
-#undef MOE_WAIT_CASE
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    return __builtin_bit_cast(bf16x8, v);
 }
 
 }  // namespace
@@ -74,132 +65,159 @@ __device__ __forceinline__ void wait_vmcnt(int n)
 struct SmallTile {
     __amdgpu_buffer_rsrc_t ra, rb;
     bf16 *C;
-    int row0, rows_valid, n0, nrb, a_cnt, N, K, KT;
+    int row0, rows_valid, n0, N, K, KT;
 };
 
 struct SmallLds {
     bf16 *a[kRing];   // token-row tiles, 192 rows x 64 bf16 each
-    bf16 *b[kRing];   // weight tiles, 128 rows x 64 bf16 each
 };
 
-// Fills of step j: token rows into a[j % 4], then weights into b[j % 4].
+// Per-wave constants: which K half and column half the wave owns, and the
+// lane's weight-load offsets.
+struct SmallWave {
+    int wave, lane, kh, ch;
+    int voff_even, voff_odd;   // token-row fills (direct to LDS)
+    int vb;                    // weight fragment (column block 2 ch, sub-step 2 kh)
+    int cbstride;              // bytes between column blocks
+};
+
+// Fills of step j: token rows into a[I] (direct to LDS), weights into the
+// register slot I; exactly NMB + 4 vector loads per wave, with no branch, so
+// that the compiler's own waits on the weight registers stay exact.  Row
+// blocks past the group read past the buffer range and return zeros; steps
+// past K re-read the last step.  Such rows and ring slots are never used.
 template <int NMB, int I>
-__device__ __forceinline__ void fill_step(const SmallTile &t, const SmallLds &l, int j, int wave,
-                                          int voff_even, int voff_odd)
+__device__ __forceinline__ void fill_step(const SmallTile &t, const SmallLds &l, const SmallWave &w,
+                                          int j, bf16x8 (&breg)[kRing][4])
 {
-    if (j >= t.KT) return;
+    const int js = min(j, t.KT - 1);
 #pragma unroll
-    for (int i = 0; i < NMB; ++i) {
-        const int blk = wave + 4 * i;
-        if (blk < t.nrb)
-            rows8_to_lds(t.ra, l.a[I], blk, voff_even, voff_odd, t.K * 2, j * kBKs * 2);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        rows8_to_lds(t.rb, l.b[I], wave * 4 + i, voff_even, voff_odd, t.K * 2, j * kBKs * 2);
+    for (int i = 0; i < NMB; ++i)
+        rows8_to_lds(t.ra, l.a[I], w.wave + 4 * i, w.voff_even, w.voff_odd, t.K * 2, js * kBKs * 2);
+    // [column block][sub-step]: q = 2 cb + m holds sub-step 2 kh + m
+    const int soff = js * 4 * 1024;
+    breg[I][0] = load_b128(t.rb, w.vb, soff);
+    breg[I][1] = load_b128(t.rb, w.vb + 1024, soff);
+    breg[I][2] = load_b128(t.rb, w.vb + w.cbstride, soff);
+    breg[I][3] = load_b128(t.rb, w.vb + w.cbstride + 1024, soff);
 }
 
 // One K step with compile-time ring index I = k % 4.
 template <int NMB, int I>
 __device__ __forceinline__ void small_step(const SmallTile &t, const SmallLds &l,
-                                           f32x16 (&acc)[NMB], int k, int wave, int lane,
-                                           int voff_even, int voff_odd)
+                                           const SmallWave &w, f32x16 (&acc)[NMB][2], int k,
+                                           bf16x8 (&breg)[kRing][4])
 {
-    // Fills are issued in step order (rows j, weights j, rows j+1, ...) and
-    // steps k+1 and k+2 are the ones already issued after step k's.
-    wait_vmcnt((t.a_cnt + 4) * min(2, t.KT - 1 - k));
+    // The fills of steps k+1 and k+2 are the loads issued after step k's.
+    constexpr int kAfter = 2 * (NMB + 4);
+    __builtin_amdgcn_s_waitcnt((kAfter & 15) | ((kAfter >> 4) << 14) | (7 << 4) | (15 << 8));
     __builtin_amdgcn_s_barrier();          // every wave's fills of step k landed; step k-1 read
-    fill_step<NMB, (I + 3) & 3>(t, l, k + 3, wave, voff_even, voff_odd);
+    fill_step<NMB, (I + 3) & 3>(t, l, w, k + 3, breg);
     __builtin_amdgcn_sched_barrier(0);
 
-    const int rd_row = lane & 31;
-    const int rd_hi = lane >> 5;
+    // Token-row fragment (mb, m) of sub-step kk = 2 kh + m: row
+    // 32 mb + lane % 32, 16-byte chunk 2 kk + lane / 32, stored swizzled.
+    const int rd_row = w.lane & 31;
     const int swz = (rd_row >> 1) & 7;
+    const int c0 = 4 * w.kh + (w.lane >> 5);
     const bf16 *As = l.a[I];
-    const bf16 *Bs = l.b[I];
-    // Fragments of sub-step kk+1 are read while the MFMAs of kk run.
-    auto read = [&](int kk, bf16x8 (&af)[NMB], bf16x8 &bfr) {
-        const int ch = ((kk * 2 + rd_hi) ^ swz) << 3;
-        bfr = *(const bf16x8 *)&Bs[(wave * 32 + rd_row) * kRowEs + ch];
+    bf16x8 a0[NMB], a1[NMB];
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb)
-            af[mb] = *(const bf16x8 *)&As[(mb * 32 + rd_row) * kRowEs + ch];
-    };
-    auto mma = [&](const bf16x8 (&af)[NMB], const bf16x8 &bfr) {
+    for (int mb = 0; mb < NMB; ++mb)
+        a0[mb] = *(const bf16x8 *)&As[(mb * 32 + rd_row) * kRowEs + ((c0 ^ swz) << 3)];
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb)
-            acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr, acc[mb], 0, 0, 0);
-    };
-    bf16x8 a0[NMB], a1[NMB], b0, b1;
-    read(0, a0, b0);
-    read(1, a1, b1);
+    for (int mb = 0; mb < NMB; ++mb)
+        a1[mb] = *(const bf16x8 *)&As[(mb * 32 + rd_row) * kRowEs + (((c0 + 2) ^ swz) << 3)];
     __builtin_amdgcn_sched_barrier(0);
-    mma(a0, b0);
-    read(2, a0, b0);
-    __builtin_amdgcn_sched_barrier(0);
-    mma(a1, b1);
-    read(3, a1, b1);
-    __builtin_amdgcn_sched_barrier(0);
-    mma(a0, b0);
-    mma(a1, b1);
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+        acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[mb], breg[I][0], acc[mb][0], 0, 0, 0);
+        acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[mb], breg[I][2], acc[mb][1], 0, 0, 0);
+    }
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+        acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mb], breg[I][1], acc[mb][0], 0, 0, 0);
+        acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mb], breg[I][3], acc[mb][1], 0, 0, 0);
+    }
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// One tile with NMB 32-row blocks: K loop and epilogue, fully unrolled over
-// the row blocks so no accumulator crosses a branch.
+// One tile with NMB 32-row blocks: K loop, K-half reduction and epilogue,
+// fully unrolled over the row blocks so no accumulator crosses a branch.
 template <bool SWIGLU, int NMB>
-__device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLds &l, int wave,
-                                               int lane, int voff_even, int voff_odd)
+__device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLds &l,
+                                               const SmallWave &w, float *red)
 {
-    f32x16 acc[NMB];
+    f32x16 acc[NMB][2];
 #pragma unroll
-    for (int i = 0; i < NMB; ++i) acc[i] = (f32x16){};
+    for (int i = 0; i < NMB; ++i) acc[i][0] = acc[i][1] = (f32x16){};
+    bf16x8 breg[kRing][4];
 
-    fill_step<NMB, 0>(t, l, 0, wave, voff_even, voff_odd);
-    fill_step<NMB, 1>(t, l, 1, wave, voff_even, voff_odd);
-    fill_step<NMB, 2>(t, l, 2, wave, voff_even, voff_odd);
+    fill_step<NMB, 0>(t, l, w, 0, breg);
+    fill_step<NMB, 1>(t, l, w, 1, breg);
+    fill_step<NMB, 2>(t, l, w, 2, breg);
     // K is a multiple of 128, so KT is even: groups of 4 steps, then 2.
     int k = 0;
     for (; k + 4 <= t.KT; k += 4) {
-        small_step<NMB, 0>(t, l, acc, k, wave, lane, voff_even, voff_odd);
-        small_step<NMB, 1>(t, l, acc, k + 1, wave, lane, voff_even, voff_odd);
-        small_step<NMB, 2>(t, l, acc, k + 2, wave, lane, voff_even, voff_odd);
-        small_step<NMB, 3>(t, l, acc, k + 3, wave, lane, voff_even, voff_odd);
+        small_step<NMB, 0>(t, l, w, acc, k, breg);
+        small_step<NMB, 1>(t, l, w, acc, k + 1, breg);
+        small_step<NMB, 2>(t, l, w, acc, k + 2, breg);
+        small_step<NMB, 3>(t, l, w, acc, k + 3, breg);
     }
     if (k < t.KT) {
-        small_step<NMB, 0>(t, l, acc, k, wave, lane, voff_even, voff_odd);
-        small_step<NMB, 1>(t, l, acc, k + 1, wave, lane, voff_even, voff_odd);
+        small_step<NMB, 0>(t, l, w, acc, k, breg);
+        small_step<NMB, 1>(t, l, w, acc, k + 1, breg);
     }
-    __syncthreads();   // all LDS reads done before the next tile's fills
+    __syncthreads();   // all ring reads done: the ring now holds the K-half partials
 
-    // Epilogue: register r of a 32x32 block = row 8 (r/4) + 4 (lane/32) + r%4,
-    // column lane % 32 of this wave's 32 columns.
-    const int rd_hi = lane >> 5;
-    if constexpr (SWIGLU) {
-        const int f = t.N / 2;
-        const bool gl = (lane & 16) == 0;
-        const int hc = (t.n0 + wave * 32) / 2 + (lane & 15);
+    // wave (1, ch) hands its partial sums to wave (0, ch), lane-contiguous
+    float *part = red + w.ch * (NMB * 2 * 16 * 64);
+    if (w.kh == 1) {
 #pragma unroll
         for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float v = acc[mb][r];
-                const float up = __shfl_xor(v, 16);
-                const int lr = mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
-                if (gl && lr < t.rows_valid)
-                    t.C[(int64_t)(t.row0 + lr) * f + hc] = f2bf(v / (1.0f + __expf(-v)) * up);
-            }
-    } else {
-        const int col = t.n0 + wave * 32 + (lane & 31);
+            for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    part[((mb * 2 + cb) * 16 + r) * 64 + w.lane] = acc[mb][cb][r];
+    }
+    __syncthreads();
+    if (w.kh == 0) {
+        // Epilogue, one 32x32 block at a time: register r of a block = row
+        // 8 (r/4) + 4 (lane/32) + r%4, column lane % 32 of the block.
+        const int rd_hi = w.lane >> 5;
 #pragma unroll
         for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int lr = mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
-                if (lr < t.rows_valid && col < t.N)
-                    t.C[(int64_t)(t.row0 + lr) * t.N + col] = f2bf(acc[mb][r]);
+            for (int cb = 0; cb < 2; ++cb) {
+                f32x16 v = acc[mb][cb];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) v[r] += part[((mb * 2 + cb) * 16 + r) * 64 + w.lane];
+                const int cbase = t.n0 + w.ch * 64 + cb * 32;
+                if constexpr (SWIGLU) {
+                    const int f = t.N / 2;
+                    const bool gl = (w.lane & 16) == 0;
+                    const int hc = cbase / 2 + (w.lane & 15);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const float up = __shfl_xor(v[r], 16);
+                        const int lr = mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
+                        if (gl && lr < t.rows_valid)
+                            t.C[(int64_t)(t.row0 + lr) * f + hc] =
+                                f2bf(v[r] / (1.0f + __expf(-v[r])) * up);
+                    }
+                } else {
+                    const int col = cbase + (w.lane & 31);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int lr = mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
+                        if (lr < t.rows_valid && col < t.N)
+                            t.C[(int64_t)(t.row0 + lr) * t.N + col] = f2bf(v[r]);
+                    }
+                }
             }
     }
+    __syncthreads();   // partials read before the next tile's fills reuse the ring
 }
 
 template <bool SWIGLU>
@@ -210,24 +228,30 @@ void k_gemm_bf16_small(GemmArgs a)
     __shared__ __attribute__((aligned(1024))) bf16 lds_a1[kSmallRows * kRowEs];
     __shared__ __attribute__((aligned(1024))) bf16 lds_a2[kSmallRows * kRowEs];
     __shared__ __attribute__((aligned(1024))) bf16 lds_a3[kSmallRows * kRowEs];
-    __shared__ __attribute__((aligned(1024))) bf16 lds_b0[kTNs * kRowEs];         // 4 x 16 KB
-    __shared__ __attribute__((aligned(1024))) bf16 lds_b1[kTNs * kRowEs];
-    __shared__ __attribute__((aligned(1024))) bf16 lds_b2[kTNs * kRowEs];
-    __shared__ __attribute__((aligned(1024))) bf16 lds_b3[kTNs * kRowEs];
-    const SmallLds l{{lds_a0, lds_a1, lds_a2, lds_a3}, {lds_b0, lds_b1, lds_b2, lds_b3}};
+    const SmallLds l{{lds_a0, lds_a1, lds_a2, lds_a3}};
+    // K-half partials after the K loop: 2 x (6 x 2 x 16 x 64) floats = 96 KB,
+    // which is exactly the ring; the four buffers are declared back to back.
+    static_assert(2 * 6 * 2 * 16 * 64 * 4 == 4 * kSmallRows * kRowEs * 2, "partials = ring");
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    SmallWave w;
+    w.lane = tid & 63;
+    w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    w.kh = w.wave >> 1;
+    w.ch = w.wave & 1;
     const int N = a.N, K = a.K;
     const int NT = (N + kTNs - 1) / kTNs;
     const int total = __builtin_amdgcn_readfirstlane(a.groups.st_base[a.G] * NT);
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
 
-    const int drow = lane >> 3;
-    const int voff_even = drow * K * 2 + (((lane & 7) ^ ((lane >> 4) & 7)) << 4);
-    const int voff_odd = drow * K * 2 + (((lane & 7) ^ ((4 + (lane >> 4)) & 7)) << 4);
+    const int drow = w.lane >> 3;
+    w.voff_even = drow * K * 2 + (((w.lane & 7) ^ ((w.lane >> 4) & 7)) << 4);
+    w.voff_odd = drow * K * 2 + (((w.lane & 7) ^ ((4 + (w.lane >> 4)) & 7)) << 4);
+    // fragment-order weights: column block cb of the tile starts at
+    // cb * cbstride, sub-step kk of a step at kk KB
+    w.cbstride = (K / 16) * 1024;
+    w.vb = 2 * w.ch * w.cbstride + 2 * w.kh * 1024 + w.lane * 16;
 
     for (int L = first; L < total; L += P) {
         // tile L: j-th small group, column block nt (an expert's column
@@ -244,8 +268,6 @@ void k_gemm_bf16_small(GemmArgs a)
         t.rows_valid = __builtin_amdgcn_readfirstlane(a.groups.rows[g]);
         t.row0 = __builtin_amdgcn_readfirstlane(a.groups.row0[g]);
         t.n0 = nt * kTNs;
-        t.nrb = (t.rows_valid + 7) >> 3;
-        t.a_cnt = max(0, (t.nrb - wave + 3) >> 2);   // row fills this wave issues per step
         t.N = N;
         t.K = K;
         t.KT = K / kBKs;
@@ -255,13 +277,14 @@ void k_gemm_bf16_small(GemmArgs a)
         t.ra = rsrc_s(A, (int64_t)t.rows_valid * K * 2);
         t.rb = rsrc_s(B, (int64_t)min(kTNs, N - t.n0) * K * 2);
         t.C = (bf16 *)(sh ? a.C_shared : a.C_routed);
+        float *red = (float *)lds_a0;
         switch ((t.rows_valid + 31) >> 5) {   // 32-row blocks holding rows: 1..6
-        case 1: run_small_tile<SWIGLU, 1>(t, l, wave, lane, voff_even, voff_odd); break;
-        case 2: run_small_tile<SWIGLU, 2>(t, l, wave, lane, voff_even, voff_odd); break;
-        case 3: run_small_tile<SWIGLU, 3>(t, l, wave, lane, voff_even, voff_odd); break;
-        case 4: run_small_tile<SWIGLU, 4>(t, l, wave, lane, voff_even, voff_odd); break;
-        case 5: run_small_tile<SWIGLU, 5>(t, l, wave, lane, voff_even, voff_odd); break;
-        default: run_small_tile<SWIGLU, 6>(t, l, wave, lane, voff_even, voff_odd); break;
+        case 1: run_small_tile<SWIGLU, 1>(t, l, w, red); break;
+        case 2: run_small_tile<SWIGLU, 2>(t, l, w, red); break;
+        case 3: run_small_tile<SWIGLU, 3>(t, l, w, red); break;
+        case 4: run_small_tile<SWIGLU, 4>(t, l, w, red); break;
+        case 5: run_small_tile<SWIGLU, 5>(t, l, w, red); break;
+        default: run_small_tile<SWIGLU, 6>(t, l, w, red); break;
         }
     }
 }

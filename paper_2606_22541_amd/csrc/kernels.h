@@ -16,7 +16,6 @@ struct DispatchArgs {
     int32_t *blk_counts;     // [nb][E]
     int32_t *counts;         // [E]
     int32_t *offsets;        // [E_loc+1]
-    int32_t *blk_base;       // [nb][E_loc]
     GroupTable groups;       // G = E_loc + has_shared groups
     int32_t *slot_of_row;    // [cap]
     int32_t *row_of_slot;    // [T*k]
@@ -101,6 +100,12 @@ constexpr int kInterleaveFp8 = 32;
 hipError_t launch_pack_gate_up(const void *gate, const void *up, void *packed, int32_t n_mats,
                                int32_t f, int32_t d, int32_t elem_bytes, int32_t interleave,
                                hipStream_t s);
+// bf16 weights in MFMA fragment order (the layout both bf16 grouped-GEMM
+// kernels read B in): chunk ((m * N/32 + n/32) * K/16 + k/16) * 64 + n % 32 +
+// 32 ((k/8) % 2) of 16 bytes holds row n, columns k..k+7 (k % 8 == 0).  With
+// `up` non-null the packed rows interleave gate and up by `interleave`.
+hipError_t launch_pack_frag_bf16(const void *gate, const void *up, void *dst, int32_t n_mats,
+                                 int32_t N, int32_t K, int32_t interleave, hipStream_t s);
 // Per-32-row scales of the packed matrix from the 128x128 block scales:
 // packed_s[m][p32][kb] = (gate or up)_s[m][(32*b)/128][kb].
 hipError_t launch_pack_gate_up_scales(const float *gs, const float *us, float *packed_s,

@@ -124,4 +124,47 @@ hipError_t launch_pack_gate_up_scales(const float *gs, const float *us, float *p
     return hipGetLastError();
 }
 
+// bf16 weights in MFMA fragment order.  Row n (of N) and column k (of K) of
+// matrix m go to 16-byte chunk ((m * N/32 + n/32) * K/16 + k/16) * 64 + lane,
+// element k % 8, with lane = n % 32 + 32 * ((k / 8) % 2): the 64 lanes'
+// operands of one 32-column x 16-K B fragment of v_mfma_f32_32x32x16_bf16
+// are 1 KB of consecutive memory, and a column block's fragments follow
+// each other along K.  With `up` given, packed row n interleaves gate and up
+// rows in blocks of `il` (N = 2 f rows per matrix).
+__global__ void k_pack_frag_bf16(const uint4 *__restrict__ gate, const uint4 *__restrict__ up,
+                                 uint4 *__restrict__ dst, int32_t n_mats, int32_t N, int32_t K,
+                                 int32_t il)
+{
+    const int64_t total = (int64_t)n_mats * N * (K / 8);
+    const int kc = K / 16, nbs = N / 32, row_vecs = K / 8;
+    const int rows_per_src = up ? N / 2 : N;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int lane = (int)(q & 63);
+        int64_t rest = q >> 6;
+        const int kk = (int)(rest % kc);
+        rest /= kc;
+        const int nb = (int)(rest % nbs);
+        const int m = (int)(rest / nbs);
+        const int n = nb * 32 + (lane & 31);
+        const int kv = kk * 2 + (lane >> 5);           // 8-element chunk along K
+        const uint4 *src = gate;
+        int srow = n;
+        if (up) {
+            const int b = n / (2 * il), i = n % (2 * il);
+            src = (i < il) ? gate : up;
+            srow = b * il + (i % il);
+        }
+        dst[q] = src[((int64_t)m * rows_per_src + srow) * row_vecs + kv];
+    }
+}
+
+hipError_t launch_pack_frag_bf16(const void *gate, const void *up, void *dst, int32_t n_mats,
+                                 int32_t N, int32_t K, int32_t interleave, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_pack_frag_bf16, dim3(4096), dim3(256), 0, s, (const uint4 *)gate,
+                       (const uint4 *)up, (uint4 *)dst, n_mats, N, K, interleave);
+    return hipGetLastError();
+}
+
 }  // namespace moe

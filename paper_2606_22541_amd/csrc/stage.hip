@@ -20,7 +20,7 @@ using namespace moe;
 namespace {
 
 struct SlotWs {
-    int32_t *blk_counts = nullptr, *counts = nullptr, *offsets = nullptr, *blk_base = nullptr;
+    int32_t *blk_counts = nullptr, *counts = nullptr, *offsets = nullptr;
     int32_t *g_row0 = nullptr, *g_rows = nullptr, *g_mt_base = nullptr;
     int32_t *g_lt_base = nullptr, *g_st_base = nullptr;
     int32_t *slot_of_row = nullptr, *row_of_slot = nullptr;
@@ -175,13 +175,15 @@ struct ProfScope {
     hipEvent_t a = nullptr;
     ProfScope(moe_stage *st_, int kind_, hipStream_t s_) : st(st_), kind(kind_), s(s_)
     {
-        if (st->prof_on && hipEventCreate(&a) == hipSuccess) hipEventRecord(a, s);
+        if (st->prof_on && hipEventCreateWithFlags(&a, hipEventDisableSystemFence) == hipSuccess)
+            hipEventRecord(a, s);
     }
     ~ProfScope()
     {
         if (!a) return;
         hipEvent_t b = nullptr;
-        if (hipEventCreate(&b) == hipSuccess && hipEventRecord(b, s) == hipSuccess)
+        if (hipEventCreateWithFlags(&b, hipEventDisableSystemFence) == hipSuccess &&
+            hipEventRecord(b, s) == hipSuccess)
             st->prof.push_back(ProfRec{kind, a, b});
         else
             hipEventDestroy(a);
@@ -254,22 +256,38 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
         release(st);
         return MOE_ENOMEM;
     }
-    // Pack the weights: [gate|up] interleaved by 32 rows, down as is; the
-    // shared expert is group E_loc.
+    // Pack the weights; the shared expert is group E_loc.  bf16: [gate|up]
+    // interleaved by 16 rows and down, both in MFMA fragment order.  fp8:
+    // [gate|up] interleaved by 32 rows (row-major), down as is.
     hipError_t e = hipSuccess;
     const int64_t w1_mat = 2 * F * D * z.eb, w2_mat = D * F * z.eb;
-    const int32_t il = fp8 ? kInterleaveFp8 : kInterleaveBf16;
-    e = launch_pack_gate_up(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)F, (int32_t)D,
-                            (int32_t)z.eb, il, st->own);
-    if (e == hipSuccess)
-        e = hipMemcpyAsync(st->w2, w->w_down, (size_t)(El * w2_mat), hipMemcpyDeviceToDevice,
-                           st->own);
-    if (e == hipSuccess && desc->has_shared_expert) {
-        e = launch_pack_gate_up(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
-                                (int32_t)F, (int32_t)D, (int32_t)z.eb, il, st->own);
+    if (fp8) {
+        e = launch_pack_gate_up(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)F, (int32_t)D,
+                                (int32_t)z.eb, kInterleaveFp8, st->own);
         if (e == hipSuccess)
-            e = hipMemcpyAsync((char *)st->w2 + El * w2_mat, w->sh_down, (size_t)w2_mat,
-                               hipMemcpyDeviceToDevice, st->own);
+            e = hipMemcpyAsync(st->w2, w->w_down, (size_t)(El * w2_mat), hipMemcpyDeviceToDevice,
+                               st->own);
+        if (e == hipSuccess && desc->has_shared_expert) {
+            e = launch_pack_gate_up(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
+                                    (int32_t)F, (int32_t)D, (int32_t)z.eb, kInterleaveFp8,
+                                    st->own);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync((char *)st->w2 + El * w2_mat, w->sh_down, (size_t)w2_mat,
+                                   hipMemcpyDeviceToDevice, st->own);
+        }
+    } else {
+        e = launch_pack_frag_bf16(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)(2 * F),
+                                  (int32_t)D, kInterleaveBf16, st->own);
+        if (e == hipSuccess)
+            e = launch_pack_frag_bf16(w->w_down, nullptr, st->w2, (int32_t)El, (int32_t)D,
+                                      (int32_t)F, 0, st->own);
+        if (e == hipSuccess && desc->has_shared_expert) {
+            e = launch_pack_frag_bf16(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
+                                      (int32_t)(2 * F), (int32_t)D, kInterleaveBf16, st->own);
+            if (e == hipSuccess)
+                e = launch_pack_frag_bf16(w->sh_down, nullptr, (char *)st->w2 + El * w2_mat, 1,
+                                          (int32_t)D, (int32_t)F, 0, st->own);
+        }
     }
     if (e == hipSuccess && fp8) {
         const int64_t s1_mat = (2 * F / 32) * (D / 128), s2_mat = (D / 128) * (F / 128);
@@ -297,7 +315,7 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
     const int64_t T1 = desc->max_tokens > 0 ? desc->max_tokens : 1;
     for (auto &sl : st->slots) {
         ok = alloc(st, &sl.blk_counts, z.nb_max * E * 4) && alloc(st, &sl.counts, E * 4) &&
-             alloc(st, &sl.offsets, (El + 1) * 4) && alloc(st, &sl.blk_base, z.nb_max * El * 4) &&
+             alloc(st, &sl.offsets, (El + 1) * 4) &&
              alloc(st, &sl.g_row0, z.G * 4) && alloc(st, &sl.g_rows, z.G * 4) &&
              alloc(st, &sl.g_mt_base, (z.G + 1) * 4) && alloc(st, &sl.g_lt_base, (z.G + 1) * 4) &&
              alloc(st, &sl.g_st_base, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
@@ -317,7 +335,7 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
             release(st);
             return MOE_ENOMEM;
         }
-        if (hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming) != hipSuccess) {
+        if (hipEventCreateWithFlags(&sl.ev, hipEventDisableTiming | hipEventDisableSystemFence) != hipSuccess) {
             release(st);
             return MOE_EHIP;
         }
@@ -345,7 +363,11 @@ static bool mb_ok(const moe_stage *st, const moe_microbatch *mb)
     return true;
 }
 
-moe_status moe_dispatch(moe_stage *st, int32_t slot, const moe_microbatch *mb, void *stream)
+// The three phases.  `rec` records the slot's event at the end; a submit
+// records it once, after the combine, since every record is a release that
+// stalls the stream for several microseconds.
+static moe_status dispatch_impl(moe_stage *st, int32_t slot, const moe_microbatch *mb,
+                                void *stream, bool rec)
 {
     if (!slot_ok(st, slot) || !mb_ok(st, mb)) return MOE_EINVAL;
     const moe_stage_desc &d = st->desc;
@@ -368,7 +390,6 @@ moe_status moe_dispatch(moe_stage *st, int32_t slot, const moe_microbatch *mb, v
     a.blk_counts = sl.blk_counts;
     a.counts = sl.counts;
     a.offsets = sl.offsets;
-    a.blk_base = sl.blk_base;
     a.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base};
     a.slot_of_row = sl.slot_of_row;
     a.row_of_slot = sl.row_of_slot;
@@ -391,10 +412,10 @@ moe_status moe_dispatch(moe_stage *st, int32_t slot, const moe_microbatch *mb, v
                                     s) != hipSuccess)
             return MOE_EHIP;
     }
-    return record(sl, s);
+    return rec ? record(sl, s) : MOE_OK;
 }
 
-moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
+static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
 {
     if (!slot_ok(st, slot)) return MOE_EINVAL;
     SlotWs &sl = st->slots[slot];
@@ -402,7 +423,7 @@ moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
     const moe_stage_desc &d = st->desc;
     const int32_t T = sl.mb.n_tokens;
     hipStream_t s = (hipStream_t)stream;
-    if (T == 0) return record(sl, s);
+    if (T == 0) return rec ? record(sl, s) : MOE_OK;
     const bool fp8 = d.dtype == MOE_DTYPE_FP8_E4M3_B128;
     const int64_t max_rows = (int64_t)T * d.top_k;
     int64_t mt_max = (max_rows + kBM - 1) / kBM + d.n_local_experts;
@@ -472,10 +493,10 @@ moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
     }
     if (e == hipErrorNotSupported) return MOE_EUNSUPPORTED;
     if (e != hipSuccess) return MOE_EHIP;
-    return record(sl, s);
+    return rec ? record(sl, s) : MOE_OK;
 }
 
-moe_status moe_combine(moe_stage *st, int32_t slot, void *stream)
+static moe_status combine_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
 {
     if (!slot_ok(st, slot)) return MOE_EINVAL;
     SlotWs &sl = st->slots[slot];
@@ -496,7 +517,22 @@ moe_status moe_combine(moe_stage *st, int32_t slot, void *stream)
         ProfScope ps(st, 4, s);
         if (launch_combine(c, st->num_cus, s) != hipSuccess) return MOE_EHIP;
     }
-    return record(sl, s);
+    return rec ? record(sl, s) : MOE_OK;
+}
+
+moe_status moe_dispatch(moe_stage *st, int32_t slot, const moe_microbatch *mb, void *stream)
+{
+    return dispatch_impl(st, slot, mb, stream, true);
+}
+
+moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
+{
+    return ffn_impl(st, slot, stream, true);
+}
+
+moe_status moe_combine(moe_stage *st, int32_t slot, void *stream)
+{
+    return combine_impl(st, slot, stream, true);
 }
 
 moe_status moe_stage_submit_microbatch(moe_stage *st, const moe_microbatch *mb, void *stream,
@@ -509,11 +545,11 @@ moe_status moe_stage_submit_microbatch(moe_stage *st, const moe_microbatch *mb, 
     // Backpressure: the slot's previous micro-batch must be done before its
     // workspace is reused.  The wait is on the device, for that one event.
     if (sl.ev_recorded && hipStreamWaitEvent(s, sl.ev, 0) != hipSuccess) return MOE_EHIP;
-    moe_status r = moe_dispatch(st, slot, mb, stream);
+    moe_status r = dispatch_impl(st, slot, mb, stream, false);
     if (r != MOE_OK) return r;
     st->next_slot = (slot + 1) % (int32_t)st->slots.size();
-    if ((r = moe_expert_ffn(st, slot, stream)) != MOE_OK) return r;
-    if ((r = moe_combine(st, slot, stream)) != MOE_OK) return r;
+    if ((r = ffn_impl(st, slot, stream, false)) != MOE_OK) return r;
+    if ((r = combine_impl(st, slot, stream, true)) != MOE_OK) return r;
     if (slot_out) *slot_out = slot;
     return MOE_OK;
 }
