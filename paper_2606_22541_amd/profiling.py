@@ -28,22 +28,28 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = {
-    "gemm_gate_up_swiglu": ["csrc/gemm_bf16.hip", "csrc/common.h", "csrc/kernels.h"],
+    "gemm_gate_up_swiglu": ["csrc/gemm_bf16.hip", "csrc/gemm_bf16_small.hip", "csrc/common.h",
+                            "csrc/kernels.h"],
     "gemm_down": ["csrc/gemm_bf16.hip", "csrc/common.h", "csrc/kernels.h"],
+    "gemm_gate_up_swiglu_fp8": ["csrc/gemm_fp8.hip", "csrc/common.h", "csrc/kernels.h"],
+    "gemm_down_fp8": ["csrc/gemm_fp8.hip", "csrc/common.h", "csrc/kernels.h"],
     "combine": ["csrc/combine.hip", "csrc/common.h", "csrc/kernels.h"],
     "gather": ["csrc/dispatch.hip", "csrc/common.h", "csrc/kernels.h"],
+    "dispatch_index": ["csrc/dispatch.hip", "csrc/common.h", "csrc/kernels.h"],
 }
-# rocprof kernel-name prefixes of the stage's kernels -> bench kernel kinds
+# rocprof kernel-name prefixes of the stage's kernels -> the kernel groups
+# bench.py times (a group's kernels each run once per micro-batch, so a
+# group's per-step figure is the sum over its kernels)
 NAME_MAP = (
+    ("void moe::k_gemm_bf16_small<true>", "gemm_gate_up_swiglu"),
     ("void moe::k_gemm_bf16<true>", "gemm_gate_up_swiglu"),
     ("void moe::k_gemm_bf16<false>", "gemm_down"),
     ("void moe::k_gemm_fp8<true>", "gemm_gate_up_swiglu_fp8"),
     ("void moe::k_gemm_fp8<false>", "gemm_down_fp8"),
     ("moe::k_combine", "combine"),
-    ("moe::k_gather", "gather"),
-    ("moe::k_hist", "hist"),
-    ("moe::k_scan", "scan"),
-    ("moe::k_scatter", "scatter"),
+    ("void moe::k_gather", "gather"),
+    ("moe::k_hist", "dispatch_index"),
+    ("moe::k_place", "dispatch_index"),
     ("moe::k_quantize_fp8", "quantize_fp8"),
 )
 COPY_NAMES = ("__amd_rocclr_copyBuffer",)
@@ -74,21 +80,29 @@ def _find_csv(path: str, suffix: str) -> str:
 
 
 def kernel_stats(path: str):
+    """Per kernel group: calls of its first kernel and the summed average
+    and total durations of its kernels."""
     rows = list(csv.DictReader(open(_find_csv(path, "kernel_stats.csv"))))
     out = {}
     for r in rows:
         k = kind_of(r["Name"])
-        if k:
-            out[k] = {"calls": int(r["Calls"]), "avg_ms": float(r["AverageNs"]) / 1e6,
-                      "total_ms": float(r["TotalDurationNs"]) / 1e6}
+        if not k:
+            continue
+        e = out.setdefault(k, {"calls": int(r["Calls"]), "avg_ms": 0.0, "total_ms": 0.0,
+                               "kernels": []})
+        e["avg_ms"] += float(r["AverageNs"]) / 1e6
+        e["total_ms"] += float(r["TotalDurationNs"]) / 1e6
+        e["kernels"].append(r["Name"].split("(")[0])
     return out
 
 
 def counter_per_dispatch(path: str, counter: str):
-    """Mean counter value per dispatch, by kernel kind (copy kernels too)."""
+    """Mean counter value per dispatch of each kernel, summed over the
+    kernels of a group (copy kernels are their own group)."""
     rows = list(csv.DictReader(open(_find_csv(path, "counter_collection.csv"))))
     acc = collections.defaultdict(float)
     disp = collections.defaultdict(set)
+    group = {}
     for r in rows:
         if r["Counter_Name"] != counter:
             continue
@@ -96,9 +110,14 @@ def counter_per_dispatch(path: str, counter: str):
         k = kind_of(name) or (name if name in COPY_NAMES else None)
         if k is None:
             continue
-        acc[k] += float(r["Counter_Value"])
-        disp[k].add(r["Dispatch_Id"])
-    return {k: acc[k] / len(disp[k]) for k in acc}
+        key = name.split("(")[0]
+        group[key] = k
+        acc[key] += float(r["Counter_Value"])
+        disp[key].add(r["Dispatch_Id"])
+    out = collections.defaultdict(float)
+    for key, k in group.items():
+        out[k] += acc[key] / len(disp[key])
+    return dict(out)
 
 
 def traffic(args):
