@@ -2,14 +2,17 @@
 
 One step = one micro-batch through the whole stage (dispatch, grouped GEMM
 gate/up + SiLU*up, grouped GEMM down, combine) via
-moe_stage_submit_microbatch, inputs already resident in HBM.
+moe_stage_submit_microbatch, inputs already resident in HBM.  Workloads with
+several micro-batches run each on its own stream, and a step is all of them.
 
 Prints ONE JSON line.  `value` is tokens/s of the primary workload
 (DeepSeek-V3-shaped EP32 share, T=4096, 8 of 256 experts local, top-8).
-The same line carries the same measurement at T=32768 (about 1024 token-slots
-per local expert, where the grouped GEMM is compute-bound), per-kernel times
-from HIP events recorded by the library on the launch stream, the roofline
-of the dominant kernel, and the CPU oracle's throughput on the host.
+The same line carries the further workloads (T=32768, where the grouped GEMM
+is compute-bound; the EP8 share with a shared expert; four skewed ragged
+micro-batches on four streams in bf16 and fp8), per-kernel times from HIP
+events recorded by the library on the launch streams, the roofline of the
+dominant kernel, the spread of the step time over repeated regions, and the
+CPU oracle's throughput on the host.
 """
 from __future__ import annotations
 
@@ -66,65 +69,108 @@ def stream_accounting(cfg, counts_local, n_tokens_with_local, T):
     return dict(gather_bytes=gather, combine_bytes=combine)
 
 
-def run_workload(name, steps, warmup, n_buffers=3):
+def run_workload(name, steps, warmup, n_buffers=3, repeats=5):
+    """Times `steps` steps of workload `name`.  One step is every micro-batch
+    of the workload through the stage; micro-batch i runs on its own stream,
+    all of them released by one start event and joined at the end (a single
+    micro-batch runs on one stream with nothing else on it).  Returns the
+    timed region of exactly `steps` steps, the step times of `repeats`
+    further regions (spread only), and per-kernel times from the library's
+    events in one more region."""
     import torch
     from paper_2606_22541_amd import inputs
     from paper_2606_22541_amd import moe_stage as C
-    from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
+    from paper_2606_22541_amd.stage import ExpertStage, quantize_fp8, to_device_routing
 
     cfg = inputs.CONFIGS[name]
     t0 = time.time()
     w = inputs.make_weights(cfg, "cuda")
-    mb = inputs.make_microbatches(cfg, "cuda")[0]
-    T = mb.ids.shape[0]
-    _log("[bench] %s: inputs ready in %.1fs (T=%d)" % (name, time.time() - t0, T))
-    ids, wt = to_device_routing(mb.ids, mb.w)
-    # distinct input/output buffers so consecutive steps do not hit cached rows
-    bufs = []
-    for i in range(n_buffers):
-        x = mb.x.clone()
-        out = torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda")
-        bufs.append((x, ids.clone(), wt.clone(), out))
+    mbs_in = inputs.make_microbatches(cfg, "cuda")
+    n_micro = len(mbs_in)
+    Ts = [mb.ids.shape[0] for mb in mbs_in]
+    _log("[bench] %s: inputs ready in %.1fs (T=%s)" % (name, time.time() - t0, Ts))
+    # distinct input/output buffer sets so consecutive steps do not hit cached rows
+    n_sets = n_buffers if n_micro == 1 else 2
+    sets = []
+    for _ in range(n_sets):
+        one = []
+        for mb in mbs_in:
+            ids, wt = to_device_routing(mb.ids, mb.w)
+            x, xs = mb.x.clone(), None
+            if cfg.dtype == "fp8":
+                x, xs = quantize_fp8(x)        # sender-side, outside the timed region
+            out = torch.empty((mb.ids.shape[0], cfg.d), dtype=torch.bfloat16, device="cuda")
+            one.append((x, xs, ids, wt, out))
+        sets.append(one)
     torch.cuda.synchronize()
-    stage = ExpertStage(cfg, w, n_slots=2, max_tokens=T)
-    mbs = [stage.microbatch(x, i_, w_, o) for (x, i_, w_, o) in bufs]
-    stream = torch.cuda.Stream()
+    stage = ExpertStage(cfg, w, n_slots=max(2, n_micro), max_tokens=max(Ts))
+    mbs = [[stage.microbatch(x, i_, w_, o, xs) for (x, xs, i_, w_, o) in one] for one in sets]
+    main = torch.cuda.Stream()
+    streams = [torch.cuda.Stream() for _ in range(n_micro)] if n_micro > 1 else [main]
+
+    def step(s):
+        group = mbs[s % n_sets]
+        if n_micro == 1:
+            stage.submit(group[0], main)
+            return
+        go = torch.cuda.Event()
+        go.record(main)
+        for i, m in enumerate(group):
+            streams[i].wait_event(go)
+            stage.submit(m, streams[i])
+            done = torch.cuda.Event()
+            done.record(streams[i])
+            main.wait_event(done)
+
+    def region(n):
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(main)
+        for s in range(n):
+            step(s)
+        end.record(main)
+        stage.sync()
+        torch.cuda.synchronize()
+        return start.elapsed_time(end)
+
     for s in range(warmup):
-        stage.submit(mbs[s % n_buffers], stream)
+        step(s)
     stage.sync()
     torch.cuda.synchronize()
-    # timed region 1: the step rate, nothing but the stage on the stream
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for s in range(steps):
-        stage.submit(mbs[s % n_buffers], stream)
-    end.record(stream)
-    stage.sync()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end)
-    # timed region 2: the same steps with the library's per-kernel HIP events
+    ms = region(steps)                                  # timed region: exactly `steps` steps
+    spread = sorted([ms / steps] + [region(steps) / steps for _ in range(repeats)])
+    # per-kernel times: the same steps with the library's HIP events
     C.moe_stage_profile(stage.handle, True)
     for s in range(steps):
-        stage.submit(mbs[s % n_buffers], stream)
+        step(s)
     stage.sync()
     torch.cuda.synchronize()
     prof = C.moe_stage_profile_read(stage.handle)
     C.moe_stage_profile(stage.handle, False)
     stage.close()
 
-    counts = np.bincount(mb.ids[(mb.ids >= 0)].ravel(), minlength=cfg.E)
-    counts_local = counts[cfg.e0:cfg.e0 + cfg.E_loc]
-    local = (mb.ids >= cfg.e0) & (mb.ids < cfg.e0 + cfg.E_loc)
-    n_tok_local = int(np.count_nonzero(local.any(axis=1)))
-    acct = gemm_accounting(cfg, counts_local, T)
-    acct.update(stream_accounting(cfg, counts_local, n_tok_local, T))
-    kern = {k: (v[0] / v[1] if v[1] else None) for k, v in prof.items()}
-    del w, mb, bufs
+    acct = None
+    n_local, n_tok_local = 0, 0
+    for mb in mbs_in:
+        counts = np.bincount(mb.ids[(mb.ids >= 0)].ravel(), minlength=cfg.E)
+        counts_local = counts[cfg.e0:cfg.e0 + cfg.E_loc]
+        local = (mb.ids >= cfg.e0) & (mb.ids < cfg.e0 + cfg.E_loc)
+        a = gemm_accounting(cfg, counts_local, mb.ids.shape[0])
+        a.update(stream_accounting(cfg, counts_local, int(np.count_nonzero(local.any(axis=1))),
+                                   mb.ids.shape[0]))
+        acct = a if acct is None else {k: acct[k] + a[k] for k in acct}
+        n_local += int(counts_local.sum())
+    # per-step totals (a kernel group runs once per micro-batch)
+    kern = {k: (v[0] / steps if v[1] else None) for k, v in prof.items()}
+    del w, mbs_in, sets
     torch.cuda.empty_cache()
-    return dict(cfg=cfg, T=T, ms=ms, steps=steps, kern=kern, acct=acct,
-                n_local_slots=int(counts_local.sum()))
+    return dict(cfg=cfg, T=sum(Ts), Ts=Ts, ms=ms, steps=steps, kern=kern, acct=acct,
+                n_local_slots=n_local, n_micro=n_micro,
+                spread={"p10": round(float(np.percentile(spread, 10)), 4),
+                        "p50": round(float(np.percentile(spread, 50)), 4),
+                        "p90": round(float(np.percentile(spread, 90)), 4),
+                        "regions": len(spread)})
 
 
 def measured_traffic(workload, kernel):
@@ -142,6 +188,8 @@ def measured_traffic(workload, kernel):
 
 
 def roofline_for(r, kernel="gemm_gate_up_swiglu"):
+    """Roofline of one launch of `kernel` (per step when the step has one
+    micro-batch; summed over the step's micro-batches otherwise)."""
     a = r["acct"]
     t = r["kern"][kernel] / 1e3
     flop, byts = (a["g1_flop"], a["g1_bytes"]) if kernel == "gemm_gate_up_swiglu" else (
@@ -164,25 +212,46 @@ def roofline_for(r, kernel="gemm_gate_up_swiglu"):
 
 
 def stream_rooflines(r):
+    """Per-step time of each kernel group (summed over the step's micro-batches)
+    against its algorithmic bytes or FLOPs."""
     a = r["acct"]
+    peak_tf = PEAK_FP8_TFLOPS if r["cfg"].dtype == "fp8" else PEAK_BF16_TFLOPS
+    g1k, g2k = "gemm_gate_up_swiglu", "gemm_down"
     out = {}
     for k, b in (("gather", a["gather_bytes"]), ("combine", a["combine_bytes"])):
-        t = r["kern"][k]
+        t = r["kern"].get(k)
         if t:
             gbs = b / (t / 1e3) / 1e9
             out[k] = {"avg_ms": round(t, 4), "algorithmic_bytes": b, "achieved_GBs": round(gbs, 1),
                       "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
-    g1, g2 = r["kern"]["gemm_gate_up_swiglu"], r["kern"]["gemm_down"]
-    out["gemm_gate_up_swiglu"] = {"avg_ms": round(g1, 4),
-                                  "tflops": round(a["g1_flop"] / (g1 / 1e3) / 1e12, 1)}
-    out["gemm_down"] = {"avg_ms": round(g2, 4),
-                        "tflops": round(a["g2_flop"] / (g2 / 1e3) / 1e12, 1)}
-    out["grouped_gemm_total"] = {
-        "tflops": round((a["g1_flop"] + a["g2_flop"]) / ((g1 + g2) / 1e3) / 1e12, 1),
-        "frac_mfma": round((a["g1_flop"] + a["g2_flop"]) / ((g1 + g2) / 1e3) / 1e12
-                           / PEAK_BF16_TFLOPS, 4)}
+    g1, g2 = r["kern"][g1k], r["kern"][g2k]
+    out[g1k] = {"avg_ms": round(g1, 4), "tflops": round(a["g1_flop"] / (g1 / 1e3) / 1e12, 1)}
+    out[g2k] = {"avg_ms": round(g2, 4), "tflops": round(a["g2_flop"] / (g2 / 1e3) / 1e12, 1)}
+    tot = (a["g1_flop"] + a["g2_flop"]) / ((g1 + g2) / 1e3) / 1e12
+    out["grouped_gemm_total"] = {"tflops": round(tot, 1), "frac_mfma": round(tot / peak_tf, 4),
+                                 "peak_tflops": peak_tf}
+    if r["kern"].get("quantize_h"):
+        out["quantize_h"] = {"avg_ms": round(r["kern"]["quantize_h"], 4)}
     out["dispatch_index"] = {"avg_ms": round(r["kern"]["dispatch_index"], 4)}
     return out
+
+
+WORKLOAD_TEXT = {
+    "c1": "DeepSeek-V3 EP32 expert share, T=%(T)d tokens, d=%(d)d, f=%(f)d, %(El)d of %(E)d "
+          "experts local, top-%(k)d, bf16",
+    "c1p": "the c1 share at T=%(T)d (about %(per)d token-slots per local expert), bf16",
+    "c2": "c1 shapes, %(n)d micro-batches of lognormal lengths %(Ts)s on %(n)d streams, "
+          "Zipf(1.2) routing, two dead local experts, bf16",
+    "c3": "EP8 share, T=%(T)d, %(El)d of %(E)d experts local plus one shared expert, bf16",
+    "c4": "c2 in fp8 (e4m3 with 128-block scales), %(n)d micro-batches %(Ts)s on %(n)d streams",
+}
+
+
+def describe(r):
+    c = r["cfg"]
+    return "%s: " % c.name + WORKLOAD_TEXT.get(c.name, "%(T)d tokens") % dict(
+        T=r["T"], d=c.d, f=c.f, El=c.E_loc, E=c.E, k=c.k, n=r["n_micro"], Ts=r["Ts"],
+        per=r["n_local_slots"] // c.E_loc)
 
 
 def cpu_baseline(name="c1", min_seconds=10.0):
@@ -224,7 +293,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c1")
-    ap.add_argument("--secondary", default="c1p", help="'' to skip")
+    ap.add_argument("--secondary", default="c1p,c3,c2,c4",
+                    help="comma-separated further workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
@@ -264,25 +334,25 @@ def main():
         "dtype": cfg.dtype,
         "data": "synthetic (seeded; DeepSeek-V3 layer shapes, Gaussian bf16 weights, uniform "
                 "top-8 routing)",
-        "config": {"workload": "%s: DeepSeek-V3 EP32 expert share, T=%d tokens, d=%d, f=%d, "
-                               "%d of %d experts local, top-%d, bf16" % (
-                                   cfg.name, prim["T"], cfg.d, cfg.f, cfg.E_loc, cfg.E, cfg.k),
-                   "tokens_per_step": prim["T"], "local_slots": prim["n_local_slots"]},
+        "config": {"workload": describe(prim), "tokens_per_step": prim["T"],
+                   "local_slots": prim["n_local_slots"]},
+        "spread_ms_per_step": prim["spread"],
         "roofline": roofline_for(prim),
         "kernels": stream_rooflines(prim),
     }
     _log("[bench] primary done: %.3f ms/step" % ms_step)
-    if args.secondary:
-        sec = run_workload(args.secondary, max(args.steps // 2, 5), args.warmup)
-        line[args.secondary] = {
-            "workload": "%s: same share at T=%d (about %d token-slots per local expert)" % (
-                sec["cfg"].name, sec["T"], sec["n_local_slots"] // sec["cfg"].E_loc),
+    for name in [n for n in args.secondary.split(",") if n]:
+        sec = run_workload(name, max(args.steps // 2, 5), args.warmup)
+        line[name] = {
+            "workload": describe(sec),
+            "tokens_per_step": sec["T"],
             "tokens_per_s": round(sec["T"] * sec["steps"] / (sec["ms"] / 1e3), 1),
             "ms_per_step": round(sec["ms"] / sec["steps"], 4),
+            "spread_ms_per_step": sec["spread"],
             "roofline": roofline_for(sec),
             "kernels": stream_rooflines(sec),
         }
-        _log("[bench] secondary done")
+        _log("[bench] %s done" % name)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload)
         _log("[bench] cpu baseline done")
