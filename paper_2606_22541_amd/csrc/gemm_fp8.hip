@@ -130,9 +130,13 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
             for (int i = 0; i < 8; ++i) rows_to_lds(ra, lds_a[buf], wave * 8 + i, voff_even, voff_odd, K, soff);
 #pragma unroll
             for (int i = 0; i < 4; ++i) rows_to_lds(rb, lds_b[buf], wave * 4 + i, voff_even, voff_odd, K, soff);
-            if (wave == 0)   // 256 scales = 64 lanes x 16 bytes, contiguous
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)lds_s[buf], 16, lane * 16,
-                                                         kt * s_ld * 4, 0, 0);
+            // 256 scales = 64 lanes x 16 bytes, contiguous.  The step offset is
+            // in the range-checked vector offset, so on the last step the
+            // scales of rows past the group read as zero instead of past the
+            // end of the scale array.
+            if (wave == 0)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)lds_s[buf], 16,
+                                                         kt * s_ld * 4 + lane * 16, 0, 0, 0);
         };
 
         auto step = [&](int kt, int buf) {
