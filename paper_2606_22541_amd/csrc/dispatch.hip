@@ -101,24 +101,16 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
     const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int64_t wstart = (int64_t)b * kDispatchChunk + (int64_t)wave * kPerWave + lane;
 
-    // local expert index of each slot this lane owns (-1: not local / none)
-    int li[kSteps];
+    // The ids loads are issued first; the LDS set-up uses a barrier that
+    // waits for LDS stores only, so the histogram-row loads below are
+    // issued while the ids are still in flight (one latency, not two).
+    int v[kSteps];
     if (n_slots > 0) {
-        int v[kSteps];
 #pragma unroll
         for (int j = 0; j < kSteps; ++j) {
             const int64_t sl = wstart + j * 64;
             v[j] = ids[sl < n_slots ? sl : n_slots - 1];
         }
-#pragma unroll
-        for (int j = 0; j < kSteps; ++j) {
-            const int i = v[j] - e0;
-            li[j] = (wstart + j * 64 < n_slots && v[j] >= 0 && v[j] < E && i >= 0 && i < E_loc)
-                        ? i : -1;
-        }
-    } else {
-#pragma unroll
-        for (int j = 0; j < kSteps; ++j) li[j] = -1;
     }
     const int n_my = b < E ? (E - 1 - b) / (int)gridDim.x + 1 : 0;
     for (int i = tid; i < E_loc; i += kDispatchThreads) {
@@ -128,7 +120,8 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
         for (int w = 0; w < kWaves; ++w) wbase[w][i] = 0;
     }
     for (int q = tid; q < n_my; q += kDispatchThreads) cnt_my[q] = 0;
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));   // lgkmcnt(0) only
+    __builtin_amdgcn_s_barrier();
 
     // expert totals and the part of them in earlier workgroups
     {
@@ -144,6 +137,14 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
             atomicAdd(&tot[i], t);
             atomicAdd(&pre[i], p);
         }
+    }
+    // local expert index of each slot this lane owns (-1: not local / none)
+    int li[kSteps];
+#pragma unroll
+    for (int j = 0; j < kSteps; ++j) {
+        const int i = v[j] - e0;
+        li[j] = (n_slots > 0 && wstart + j * 64 < n_slots && v[j] >= 0 && v[j] < E && i >= 0 &&
+                 i < E_loc) ? i : -1;
     }
     // per-wave counts of this workgroup's slots
 #pragma unroll
