@@ -291,7 +291,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="c1")
     ap.add_argument("--secondary", default="c1p,c3,c2,c4",
                     help="comma-separated further workloads ('' for none)")

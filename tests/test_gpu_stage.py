@@ -210,3 +210,25 @@ def test_c2_skewed_four_streams():
 
 def test_c3_ep8_share_with_shared_expert():
     _case(inputs.CONFIGS["c3"], tokens=48)
+
+
+def test_max_local_experts_and_group_size_boundaries():
+    """256 local experts of 1024 (the largest tables the dispatch kernels
+    size for, a shared expert making 257 groups) with crafted group sizes
+    around the small/large GEMM boundary: 1, 33, 160, 192 and 193 rows, and
+    many empty experts."""
+    cfg = inputs.MoEConfig("maxE", d=256, f=128, E=1024, e0=512, E_loc=256, k=2, lengths=(0,),
+                           has_shared=True, seed=8)
+    rng = np.random.default_rng(8)
+    sizes = {512 + 0: 192, 512 + 1: 193, 512 + 2: 160, 512 + 3: 33, 512 + 4: 1}
+    first = np.concatenate([np.full(n, e, np.int32) for e, n in sizes.items()])
+    T = first.size                                       # 579 tokens
+    rng.shuffle(first)
+    # second choice: a non-local expert or a sparse spread over the other local experts
+    second = np.where(rng.random(T) < 0.7, rng.integers(0, 512, T),
+                      rng.integers(512 + 5, 512 + 256, T)).astype(np.int32)
+    ids = np.stack([first, second], 1)
+    x = torch.randn((T, cfg.d), generator=torch.Generator("cuda").manual_seed(2),
+                    device="cuda").to(torch.bfloat16)
+    mb = inputs.MicroBatch(x=x, ids=ids, w=rng.random((T, 2)).astype(np.float32))
+    _case(cfg, [mb])
