@@ -85,10 +85,10 @@ struct Tile {
     __amdgpu_buffer_rsrc_t ra, rb;
     int KT;
     int ncb;           // weight column blocks present in the tile (8, or fewer at N's end)
+    int va0, va1;      // token fills: offsets of rows 32 w + lane / 4 (+16), swizzled chunk
 };
 
 struct WaveConst {
-    int voff_a0, voff_a1;   // token fills: rows 32 w + lane / 4 (+16), swizzled chunk
     int voff_b;        // weight fill: lane * 16
     int cbstride;      // bytes between weight column blocks
     int a_rd;          // LDS element offset of this lane's token row (block 0)
@@ -117,7 +117,7 @@ __device__ __forceinline__ void fill(const Tile &t, const WaveConst &w, const St
     for (int i = 0; i < 2; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             t.ra, (lds_void *)(st.a + (w.wave * 32 + i * 16) * kRowElems), 16,
-            i ? w.voff_a1 : w.voff_a0, js * kBK * 2, 0, 0);
+            i ? t.va1 : t.va0, js * kBK * 2, 0, 0);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int f = w.wave * 2 + i;             // fragment of the stage: 2 cb + kk
@@ -200,8 +200,7 @@ void k_gemm_bf16(GemmArgs a)
     // token fill: lane l covers row 32 w + l / 4 (+16 for the second
     // instruction), chunk l % 4; (row / 4) % 4 = (l / 16) % 4 for both
     const int frow = w.wave * 32 + (lane >> 2);
-    w.voff_a0 = frow * K * 2 + (((lane & 3) ^ ((lane >> 4) & 3)) << 4);
-    w.voff_a1 = w.voff_a0 + 16 * K * 2;
+    const int fchunk = ((lane & 3) ^ ((lane >> 4) & 3)) << 4;
     w.voff_b = lane * 16;
     w.cbstride = (K / 16) * 1024;
     const int rd_row = lane & 31;
@@ -221,11 +220,23 @@ void k_gemm_bf16(GemmArgs a)
         const int rows_valid = min(kBM, grows - mt * kBM);
         const int n0 = nt * kBN;
         const bool sh = (g == a.shared_group);
-        const bf16 *A = (const bf16 *)(sh ? a.A_shared : a.A_routed) + (int64_t)row0 * K;
+        // routed rows of an indexed A are gathered in the token fills: tile
+        // row r is row A_index[row0 + r] / A_index_div of the whole A
+        const bool indexed = a.A_index != nullptr && !sh;
+        const bf16 *A = indexed ? (const bf16 *)a.A_routed
+                                : (const bf16 *)(sh ? a.A_shared : a.A_routed) + (int64_t)row0 * K;
         // the tile's column blocks n0/32 .. n0/32 + 7 are contiguous
         const bf16 *B = (const bf16 *)a.B + ((int64_t)g * N + n0) * K;
         Tile t;
-        t.ra = make_rsrc(A, (int64_t)rows_valid * K * 2);
+        t.ra = make_rsrc(A, (indexed ? a.A_routed_rows : (int64_t)rows_valid) * K * 2);
+        {
+            // rows past the group: an offset past every buffer range reads zero
+            const int r0 = frow, r1 = frow + 16;
+            t.va0 = r0 < rows_valid ? (indexed ? a.A_index[row0 + r0] / a.A_index_div : r0) * K * 2 + fchunk
+                                    : (int)0x80000000u;
+            t.va1 = r1 < rows_valid ? (indexed ? a.A_index[row0 + r1] / a.A_index_div : r1) * K * 2 + fchunk
+                                    : (int)0x80000000u;
+        }
         t.rb = make_rsrc(B, (int64_t)min(kBN, N - n0) * K * 2);
         t.KT = K / kBK;
         t.ncb = min(kBN, N - n0) / 32;

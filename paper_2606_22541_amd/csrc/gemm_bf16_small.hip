@@ -44,14 +44,18 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_s(const void *base, int64
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, n, 0x00020000);
 }
 
-// 8 rows x 128 B starting at row 8 rb; lane l -> row 8 rb + l / 8, physical
-// chunk l % 8 <- global chunk (l % 8) ^ ((row / 2) % 8).
-__device__ __forceinline__ void rows8_to_lds(__amdgpu_buffer_rsrc_t r, bf16 *tile, int rb,
-                                             int voff_even, int voff_odd, int row_bytes, int soff)
+// Offset a lane reads for tile row `r` (8 rows x 128 B per load; lane l ->
+// row 8 rb + l / 8, physical chunk l % 8 <- global chunk (l % 8) ^ ((row / 2)
+// % 8)).  Rows past the group get an offset past every buffer range, so they
+// read as zero; routed rows of an indexed A are gathered here: tile row r is
+// row index[row0 + r] / div of the whole A.
+__device__ __forceinline__ int token_row_offset(const int32_t *index, int div, int row0, int r,
+                                                int rows_valid, int row_bytes, int lane)
 {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_s *)(tile + rb * 8 * kRowEs), 16,
-                                             ((rb & 1) ? voff_odd : voff_even) + rb * 8 * row_bytes,
-                                             soff, 0, 0);
+    if (r >= rows_valid) return (int)0x80000000u;
+    const int chunk = ((lane & 7) ^ ((r >> 1) & 7)) << 4;
+    const int src = index ? index[row0 + r] / div : r;
+    return src * row_bytes + chunk;
 }
 
 __device__ __forceinline__ bf16x8 load_b128(__amdgpu_buffer_rsrc_t r, int voff, int soff)
@@ -66,6 +70,7 @@ struct SmallTile {
     __amdgpu_buffer_rsrc_t ra, rb;
     bf16 *C;
     int row0, rows_valid, n0, N, K, KT;
+    int avoff[6];      // token-row load offsets of this lane's row blocks wave + 4 i
 };
 
 struct SmallLds {
@@ -76,7 +81,6 @@ struct SmallLds {
 // lane's weight-load offsets.
 struct SmallWave {
     int wave, lane, kh, ch;
-    int voff_even, voff_odd;   // token-row fills (direct to LDS)
     int vb;                    // weight fragment (column block 2 ch, sub-step 2 kh)
     int cbstride;              // bytes between column blocks
 };
@@ -93,7 +97,9 @@ __device__ __forceinline__ void fill_step(const SmallTile &t, const SmallLds &l,
     const int js = min(j, t.KT - 1);
 #pragma unroll
     for (int i = 0; i < NMB; ++i)
-        rows8_to_lds(t.ra, l.a[I], w.wave + 4 * i, w.voff_even, w.voff_odd, t.K * 2, js * kBKs * 2);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            t.ra, (lds_void_s *)(l.a[I] + (w.wave + 4 * i) * 8 * kRowEs), 16, t.avoff[i],
+            js * kBKs * 2, 0, 0);
     // [column block][sub-step]: q = 2 cb + m holds sub-step 2 kh + m
     const int soff = js * 4 * 1024;
     breg[I][0] = load_b128(t.rb, w.vb, soff);
@@ -245,9 +251,6 @@ void k_gemm_bf16_small(GemmArgs a)
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
 
-    const int drow = w.lane >> 3;
-    w.voff_even = drow * K * 2 + (((w.lane & 7) ^ ((w.lane >> 4) & 7)) << 4);
-    w.voff_odd = drow * K * 2 + (((w.lane & 7) ^ ((4 + (w.lane >> 4)) & 7)) << 4);
     // fragment-order weights: column block cb of the tile starts at
     // cb * cbstride, sub-step kk of a step at kk KB
     w.cbstride = (K / 16) * 1024;
@@ -272,9 +275,16 @@ void k_gemm_bf16_small(GemmArgs a)
         t.K = K;
         t.KT = K / kBKs;
         const bool sh = (g == a.shared_group);
-        const bf16 *A = (const bf16 *)(sh ? a.A_shared : a.A_routed) + (int64_t)t.row0 * K;
+        const bool indexed = a.A_index != nullptr && !sh;
+        const bf16 *A = indexed ? (const bf16 *)a.A_routed
+                                : (const bf16 *)(sh ? a.A_shared : a.A_routed) + (int64_t)t.row0 * K;
         const bf16 *B = (const bf16 *)a.B + ((int64_t)g * N + t.n0) * K;
-        t.ra = rsrc_s(A, (int64_t)t.rows_valid * K * 2);
+        t.ra = rsrc_s(A, (indexed ? a.A_routed_rows : (int64_t)t.rows_valid) * K * 2);
+#pragma unroll
+        for (int i = 0; i < 6; ++i)
+            t.avoff[i] = token_row_offset(indexed ? a.A_index : nullptr, a.A_index_div, t.row0,
+                                          8 * (w.wave + 4 * i) + (w.lane >> 3), t.rows_valid,
+                                          K * 2, w.lane);
         t.rb = rsrc_s(B, (int64_t)min(kTNs, N - t.n0) * K * 2);
         t.C = (bf16 *)(sh ? a.C_shared : a.C_routed);
         float *red = (float *)lds_a0;

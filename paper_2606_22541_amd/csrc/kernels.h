@@ -39,7 +39,7 @@ hipError_t launch_transpose_scales(const float *src, int32_t rows, int32_t cols,
                                    int32_t ld, hipStream_t s);
 
 struct GemmArgs {
-    const void *A_routed;    // [rows][K] (rows of X_perm or H)
+    const void *A_routed;    // [rows][K] (rows of X_perm or H), or x itself when A_index is set
     const void *A_shared;    // [T][K] (x or H_shared) for group E_loc, if shared
     const float *As_routed;  // fp8: [rows][K/128] scales of A
     const float *As_shared;
@@ -54,6 +54,12 @@ struct GemmArgs {
     GroupTable groups;
     int32_t G;
     int32_t large_all;       // bf16 256x256 kernel: 1 = every group, 0 = only rows > kSmallRows
+    // bf16 only: when A_index is set, routed row r (r < the routed rows) is row
+    // A_index[r] / A_index_div of A_routed, which has A_routed_rows rows (the
+    // row gather happens in the GEMM's token-row loads; A_index = slot_of_row).
+    const int32_t *A_index;
+    int32_t A_index_div;
+    int64_t A_routed_rows;
 };
 
 // bf16 grouped GEMM.  swiglu = true: B is the packed [gate|up] matrix

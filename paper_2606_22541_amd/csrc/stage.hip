@@ -89,10 +89,9 @@ Sizes sizes_of(const moe_stage_desc *d)
     const int64_t T1 = T > 0 ? T : 1;
     int64_t b = 0;
     b += align256(s.nb_max * E * 4) + align256(E * 4) + align256((El + 1) * 4);
-    b += align256(s.nb_max * El * 4);
     b += 2 * align256(s.G * 4) + 3 * align256((s.G + 1) * 4);
     b += align256(cap1 * 4) + align256((s.n_slots_tok > 0 ? s.n_slots_tok : 1) * 4);
-    b += align256(cap1 * D * s.eb) + (fp8 ? align256(cap1 * (D / 128) * 4) : 0);
+    if (fp8) b += align256(cap1 * D) + align256(cap1 * (D / 128) * 4);   // X_perm (fp8 only)
     b += align256(cap1 * F * s.eb) + (fp8 ? align256(cap1 * (F / 128) * 4) : 0);
     b += align256(cap1 * D * 2);
     if (fp8) b += align256(cap1 * F * 2);
@@ -320,9 +319,12 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
              alloc(st, &sl.g_mt_base, (z.G + 1) * 4) && alloc(st, &sl.g_lt_base, (z.G + 1) * 4) &&
              alloc(st, &sl.g_st_base, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
              alloc(st, &sl.row_of_slot, (z.n_slots_tok > 0 ? z.n_slots_tok : 1) * 4) &&
-             alloc(st, &sl.x_perm, cap1 * D * z.eb) && alloc(st, &sl.h, cap1 * F * z.eb) &&
+             alloc(st, &sl.h, cap1 * F * z.eb) &&
              alloc(st, &sl.y_perm, cap1 * D * 2);
-        if (ok && fp8) ok = alloc(st, &sl.x_perm_s, cap1 * (D / 128) * 4) &&
+        // X_perm exists only in fp8 mode; in bf16 the gate/up GEMM gathers the
+        // token rows itself
+        if (ok && fp8) ok = alloc(st, &sl.x_perm, cap1 * D) &&
+                            alloc(st, &sl.x_perm_s, cap1 * (D / 128) * 4) &&
                             alloc(st, &sl.h_s, cap1 * (F / 128) * 4);
         if (ok && fp8) ok = alloc(st, &sl.h_bf, cap1 * F * 2);
         if (ok && desc->has_shared_expert) {
@@ -398,12 +400,13 @@ static moe_status dispatch_impl(moe_stage *st, int32_t slot, const moe_microbatc
         ProfScope ps(st, 0, s);
         if (launch_dispatch_index(a, s) != hipSuccess) return MOE_EHIP;
     }
+    // fp8: gather the e4m3 rows and their (transposed) scales into X_perm.
+    // bf16: the gate/up GEMM reads the token rows of x through slot_of_row.
     const int64_t max_rows = (int64_t)T * d.top_k;
-    if (max_rows > 0) {
+    if (fp8 && max_rows > 0) {
         ProfScope ps(st, 1, s);
-        const int32_t row_bytes = fp8 ? d.d_model : 2 * d.d_model;
-        if (launch_gather_rows(mb->x, fp8 ? mb->x_scales : nullptr, sl.slot_of_row,
-                               sl.offsets + d.n_local_experts, d.top_k, row_bytes,
+        if (launch_gather_rows(mb->x, mb->x_scales, sl.slot_of_row,
+                               sl.offsets + d.n_local_experts, d.top_k, d.d_model,
                                d.d_model / 128, sl.x_perm, sl.x_perm_s, (int32_t)st->sz.cap,
                                (int32_t)max_rows, st->num_cus, s) != hipSuccess)
             return MOE_EHIP;
@@ -430,8 +433,13 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     if (d.has_shared_expert) mt_max += (T + kBM - 1) / kBM;
 
     GemmArgs g1{};
-    g1.A_routed = sl.x_perm;
+    g1.A_routed = fp8 ? sl.x_perm : sl.mb.x;
     g1.A_shared = sl.mb.x;
+    if (!fp8) {                      // routed row r = token slot_of_row[r] / k of x
+        g1.A_index = sl.slot_of_row;
+        g1.A_index_div = d.top_k;
+        g1.A_routed_rows = T;
+    }
     g1.As_routed = sl.x_perm_s;
     g1.As_shared = sl.xsh_s;
     g1.B = st->w1;
@@ -445,6 +453,9 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     g1.G = (int32_t)st->sz.G;
 
     GemmArgs g2 = g1;
+    g2.A_index = nullptr;            // H rows are already grouped by expert
+    g2.A_index_div = 0;
+    g2.A_routed_rows = 0;
     g2.A_routed = sl.h;
     g2.A_shared = sl.h_sh;
     g2.As_routed = sl.h_s;

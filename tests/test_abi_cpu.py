@@ -58,11 +58,20 @@ def test_workspace_bytes_host_only(lib):
     # weights: 8 experts x 3 bf16 matrices of 2048 x 7168
     assert weights >= 8 * 3 * 2048 * 7168 * 2
     assert weights < 8 * 3 * 2048 * 7168 * 2 + 4096
-    # per slot: X_perm and Y_perm hold T*k rows of d bf16, H holds T*k rows of f
+    # per slot: Y_perm holds T*k rows of d bf16, H holds T*k rows of f (bf16
+    # keeps no X_perm: the gate/up GEMM gathers the token rows itself)
     rows = 32768 * 8
-    assert per_slot >= rows * (7168 * 2 * 2 + 2048 * 2)
-    fp8 = C.make_desc(7168, 2048, 256, 0, 8, 8, 32768, n_slots=1, dtype=C.MOE_DTYPE_FP8_E4M3_B128)
-    assert C.moe_stage_workspace_bytes(fp8) < one
+    assert per_slot >= rows * (7168 * 2 + 2048 * 2)
+    assert per_slot < rows * (7168 * 2 * 2 + 2048 * 2)
+    f1 = C.moe_stage_workspace_bytes(
+        C.make_desc(7168, 2048, 256, 0, 8, 8, 32768, n_slots=1, dtype=C.MOE_DTYPE_FP8_E4M3_B128))
+    f3 = C.moe_stage_workspace_bytes(
+        C.make_desc(7168, 2048, 256, 0, 8, 8, 32768, n_slots=3, dtype=C.MOE_DTYPE_FP8_E4M3_B128))
+    f_slot = (f3 - f1) // 2
+    # fp8 weights: one byte per element plus one fp32 scale per 128x128 block
+    assert 8 * 3 * 2048 * 7168 <= f1 - f_slot < weights
+    # fp8 slots also hold X_perm (T*k rows of d bytes) and its block scales
+    assert f_slot >= per_slot + rows * (7168 + 7168 // 128 * 4)
 
 
 @pytest.mark.parametrize("bad", [
