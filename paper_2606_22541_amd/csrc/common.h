@@ -48,4 +48,17 @@ __device__ __forceinline__ int lane_id() { return __lane_id(); }
 __device__ __forceinline__ bf16 f2bf(float v) { return static_cast<bf16>(v); }
 __device__ __forceinline__ float bf2f(bf16 v) { return static_cast<float>(v); }
 
+// e4m3 (OCP E4M3FN) code of v, round to nearest even.  |v| is clamped to 448
+// first, which makes the conversion saturating.
+__device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float d)
+{
+    a = fminf(fmaxf(a, -448.0f), 448.0f);
+    b = fminf(fmaxf(b, -448.0f), 448.0f);
+    c = fminf(fmaxf(c, -448.0f), 448.0f);
+    d = fminf(fmaxf(d, -448.0f), 448.0f);
+    int v = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+    v = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, v, true);
+    return (uint32_t)v;
+}
+
 }  // namespace moe

@@ -1,35 +1,57 @@
 // e4m3 grouped GEMM with DeepSeek-style block scaling (fp8 variant of the
 // expert stage): activations carry one fp32 scale per row and 128-channel
-// group, weights one fp32 scale per 128x128 block (packed gate/up weights:
-// per 32 rows).  Each K step covers exactly one 128-wide scale group:
+// group, weights one fp32 scale per 128x128 block.  Each K step covers
+// exactly one 128-wide scale group g:
 //
-//   tmp  = sum over the step of e4m3(A) * e4m3(B)     (2 x v_mfma 32x32x64 f8)
-//   acc += tmp * s_A[row, step] * s_B[col block, step]  (fp32 promotion)
+//   t    = sum over the group of e4m3(A) * e4m3(B)     (v_mfma 16x16x128 f8)
+//   acc += t * (s_A[row, g] * s_B[block, g])            (fp32 promotion)
 //
 // so the block scales are applied exactly once per group in fp32.  The
 // hardware's per-32-element power-of-two (E8M0) MFMA scales cannot express
 // these fp32 scales and are left at 1.
 //
-// Tile: 256 rows x 128 columns per workgroup, four wave64s each owning a
-// 64 x 128 block (2 x 4 MFMA blocks, fp32 accumulators in VGPRs so the
-// promotion can use them).  A, B and the A-scale column of the step stream
-// into a double-buffered LDS tile with direct-to-LDS buffer loads; the
-// A-scales of X_perm / H are stored transposed ([K/128][rows]) so one step's
-// 256 scales are one contiguous 1 KB load.  The SwiGLU epilogue writes
-// h = SiLU(gate) * up as bf16; the stage then quantises H per 128 channels.
+// Design for gfx950:
+//  * one persistent workgroup per CU walks the device-built tile list
+//    (256-row tiles, as for the bf16 path), XCD-aware tile order;
+//  * a 256x256 output tile, eight wave64s (two per SIMD, so one wave's
+//    promotion arithmetic runs beside the other's MFMAs), each owning a
+//    128x64 block as 8x4 blocks of v_mfma_scale_f32_16x16x128_f8f6f4;
+//  * the weights are packed so that every wave's 64 columns fall into one
+//    128x128 scale block: gate and up rows interleave in blocks of 64, and
+//    a 256-column tile covers gate and up rows [128 t, 128 t + 128), i.e.
+//    exactly one 128-channel group of h.  The promotion then needs one
+//    weight scale per wave and group (a scalar load) and one product per
+//    row, so it costs 1.25 VALU operations per output and group;
+//  * K advances one scale group (128 bytes) per step through a 2-deep LDS
+//    ring of 64 KB stages filled by direct-to-LDS buffer loads one step
+//    ahead: token rows as 128-byte rows whose 16-byte chunks are
+//    XOR-swizzled by (row / 2) % 8, weight fragments in MFMA fragment order
+//    (two lane-contiguous 1 KB halves per 16 x 128 fragment), and the
+//    step's 256 row scales (stored transposed, [K/128][ld], so they are one
+//    contiguous 1 KB);
+//  * rows past a group's end have an offset past every buffer range and
+//    read as zero; the scalar offset, which the range check does not cover,
+//    only moves along K (clamped to the last group) and between weight
+//    column blocks that exist;
+//  * SwiGLU mode: the up waves hand their accumulators to the gate waves
+//    through LDS, the gate waves form h = SiLU(gate) * up, round it to bf16
+//    and quantise each row's 128 channels to e4m3 with one fp32 scale (the
+//    same arithmetic as the activation quantiser), and the tile's 256 rows
+//    of 128 codes are written out through LDS as 16-byte stores.  The down
+//    product writes bf16.
 #include "kernels.h"
 
 namespace moe {
 
 namespace {
 
-constexpr int kBK8 = 128;                       // e4m3 bytes per K step (one scale group)
-constexpr int kRowB = 128;                      // LDS row bytes
-constexpr int kTM = 256, kTN = 128;
-constexpr int kWaves8 = 4;
+constexpr int kGrpB = 128;                      // K bytes per step: one scale group
+constexpr int kStage8 = kBM * kGrpB;            // one operand of one stage: 32 KB
+constexpr int kWaves8 = 8;
 constexpr int kThreads8 = 64 * kWaves8;
-constexpr int kBandM8 = 4;
+constexpr int kBand8 = 4;                       // row-tiles per raster band
 typedef __attribute__((address_space(3))) void lds_void;
+static_assert(kBM == 256 && kBN == 256, "the fp8 kernel assumes 256x256 tiles");
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc8(const void *base, int64_t bytes)
 {
@@ -48,21 +70,98 @@ __device__ __forceinline__ void decode_tile8(int L, const int32_t *__restrict__ 
     g = lo;
     const int Lg = L - mt_base[g] * NT;
     const int Mt = mt_base[g + 1] - mt_base[g];
-    const int band = Lg / (kBandM8 * NT);
-    const int r = Lg - band * kBandM8 * NT;
-    const int bm = min(kBandM8, Mt - band * kBandM8);
-    mt = band * kBandM8 + r % bm;
+    const int band = Lg / (kBand8 * NT);
+    const int r = Lg - band * kBand8 * NT;
+    const int bm = min(kBand8, Mt - band * kBand8);
+    mt = band * kBand8 + r % bm;
     nt = r / bm;
 }
 
-// rows [8 rb, 8 rb + 8) of a 128-byte-row tile; lane l fills physical chunk
-// l % 8 of row 8 rb + l / 8 with global chunk (l % 8) ^ ((row / 2) % 8).
-__device__ __forceinline__ void rows_to_lds(__amdgpu_buffer_rsrc_t r, uint8_t *tile, int rb,
-                                            int voff_even, int voff_odd, int row_bytes, int soff)
+struct Tile8 {
+    __amdgpu_buffer_rsrc_t ra, rb, rs;
+    int va[4];          // token fills: rows 32 w + 8 i + lane / 8, swizzled chunk (or past the range)
+    int KT, ncb, cbstride, s_ld;
+    const float *sbp;   // this wave's weight scale of each K group
+};
+
+struct Ring8 {
+    uint8_t *a, *b;
+    float *s;
+};
+
+// Fills of K group kg (clamped to the last), 9 loads per wave:
+//  * token rows 32 w .. 32 w + 31 as four 8-row instructions; lane l writes
+//    LDS row 32 w + 8 i + l / 8, physical chunk l % 8, with global chunk
+//    (l % 8) ^ ((row / 2) % 8);
+//  * weight fragments 2 w and 2 w + 1 of the tile's 16, both 1 KB halves;
+//  * 64 of the 256 row scales (waves w and w + 4 load the same ones).
+__device__ __forceinline__ void fill8(const Tile8 &t, const Ring8 &st, int wave, int lane, int kg)
 {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)(tile + rb * 8 * kRowB), 16,
-                                             ((rb & 1) ? voff_odd : voff_even) + rb * 8 * row_bytes,
-                                             soff, 0, 0);
+    const int ks = min(kg, t.KT - 1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(t.ra, (lds_void *)(st.a + (wave * 32 + i * 8) * kGrpB),
+                                                 16, t.va[i], ks * kGrpB, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int f = wave * 2 + (i >> 1), h = i & 1;
+        const int cb = min(f, t.ncb - 1);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(t.rb, (lds_void *)(st.b + f * 2048 + h * 1024), 16,
+                                                 lane * 16, cb * t.cbstride + ks * 2048 + h * 1024,
+                                                 0, 0);
+    }
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(t.rs, (lds_void *)(st.s + (wave & 3) * 64), 4,
+                                             (ks * t.s_ld + (wave & 3) * 64 + lane) * 4, 0, 0, 0);
+}
+
+struct Wave8 {
+    int wave, lane;
+    int a_rd0, a_rd1;   // LDS byte offsets of this lane's two token chunks (row block 0)
+    int b_rd;           // LDS byte offset of this lane's weight chunk (column block 0)
+    int s_rd;           // LDS float index of this lane's 4 row scales (row block 0)
+};
+
+// One K group: wait for its stage, sync, refill the other stage with the
+// next group, then 32 MFMAs with the promotion of each row block.
+// The weight scale of the next group is loaded before the fills, so that
+// waiting for it never waits for them.
+template <int S>
+__device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ring8 (&ring)[2],
+                                        f32x4 (&acc)[8][4], float &sb_next, int kg)
+{
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0): this group's fills landed
+    __builtin_amdgcn_s_barrier();                        // ... in every wave; the other stage is idle
+    const float sb = sb_next;
+    sb_next = t.sbp[min(kg + 1, t.KT - 1)];
+    __builtin_amdgcn_sched_barrier(0);
+    fill8(t, ring[S ^ 1], w.wave, w.lane, kg + 1);
+    __builtin_amdgcn_sched_barrier(0);
+
+    const uint8_t *As = ring[S].a;
+    const uint8_t *Bs = ring[S].b;
+    const float *Ss = ring[S].s;
+    i32x8 bfr[4];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+        const i32x4 lo = *(const i32x4 *)&Bs[w.b_rd + cb * 2048];
+        const i32x4 hi = *(const i32x4 *)&Bs[w.b_rd + cb * 2048 + 1024];
+        bfr[cb] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    }
+#pragma unroll
+    for (int rb = 0; rb < 8; ++rb) {
+        const i32x4 lo = *(const i32x4 *)&As[w.a_rd0 + rb * 16 * kGrpB];
+        const i32x4 hi = *(const i32x4 *)&As[w.a_rd1 + rb * 16 * kGrpB];
+        const i32x8 af = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const f32x4 sa = *(const f32x4 *)&Ss[w.s_rd + rb * 16];
+        f32x4 tq[4];
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+            tq[cb] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bfr[cb], (f32x4){}, 0, 0,
+                                                                      0, 127, 0, 127);
+        const f32x4 s = sa * sb;
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = tq[cb] * s + acc[rb][cb];
+    }
 }
 
 }  // namespace
@@ -71,30 +170,41 @@ template <bool SWIGLU>
 __global__ __launch_bounds__(kThreads8, 1)
 void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
 {
-    __shared__ __attribute__((aligned(1024))) uint8_t lds_a[2][kTM * kRowB];
-    __shared__ __attribute__((aligned(1024))) uint8_t lds_b[2][kTN * kRowB];
-    __shared__ __attribute__((aligned(1024))) float lds_s[2][kTM];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_a0[kStage8];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_b0[kStage8];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_a1[kStage8];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_b1[kStage8];
+    __shared__ __attribute__((aligned(256))) float lds_s0[kBM];
+    __shared__ __attribute__((aligned(256))) float lds_s1[kBM];
+    const Ring8 ring[2] = {{lds_a0, lds_b0, lds_s0}, {lds_a1, lds_b1, lds_s1}};
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    Wave8 w;
+    w.lane = tid & 63;
+    w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = w.lane;
+    const int wm = w.wave >> 2, wn = w.wave & 3;        // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
-    const int NT = (N + kTN - 1) / kTN;
+    const int NT = (N + kBN - 1) / kBN;
     const int total = __builtin_amdgcn_readfirstlane(a.groups.mt_base[a.G] * NT);
-    const int KT = K / kBK8;
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
 
-    // DMA lane mapping (rows relative to an 8-row block)
-    const int drow = lane >> 3;
-    const int voff_even = drow * K + (((lane & 7) ^ ((lane >> 4) & 7)) << 4);
-    const int voff_odd = drow * K + (((lane & 7) ^ ((4 + (lane >> 4)) & 7)) << 4);
-    // MFMA operand reads
-    const int rd_row = lane & 31;
-    const int rd_hi = lane >> 5;
-    const int swz = (rd_row >> 1) & 7;
-    const int a_rd = (wave * 64 + rd_row) * kRowB;
-    const int b_rd = rd_row * kRowB;
+    // MFMA operand reads: lane l takes row l % 16 of a 16-row block and the
+    // 32 bytes [32 (l / 16), 32 (l / 16) + 32) of its 128-byte group (the
+    // weight fragments hold the same K bytes for column l % 16).
+    {
+        const int r = lane & 15, swz = (r >> 1) & 7, c0 = 2 * (lane >> 4);
+        w.a_rd0 = (wm * 128 + r) * kGrpB + ((c0 ^ swz) << 4);
+        w.a_rd1 = (wm * 128 + r) * kGrpB + (((c0 + 1) ^ swz) << 4);
+        w.b_rd = wn * 4 * 2048 + lane * 16;
+        w.s_rd = wm * 128 + 4 * (lane >> 4);
+    }
+    // token fills: lane l covers row 32 w + 8 i + l / 8, physical chunk l % 8;
+    // ((row / 2) % 8) = (4 (i % 2) + l / 16) % 8
+    const int frow = w.wave * 32 + (lane >> 3);
+    const int fch_even = ((lane & 7) ^ ((lane >> 4) & 7)) << 4;
+    const int fch_odd = ((lane & 7) ^ ((4 + (lane >> 4)) & 7)) << 4;
 
     for (int L = first; L < total; L += P) {
         int g, mt, nt;
@@ -103,147 +213,141 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
         mt = __builtin_amdgcn_readfirstlane(mt);
         nt = __builtin_amdgcn_readfirstlane(nt);
         const int grows = __builtin_amdgcn_readfirstlane(a.groups.rows[g]);
-        const int row0 = __builtin_amdgcn_readfirstlane(a.groups.row0[g]) + mt * kTM;
-        const int rows_valid = min(kTM, grows - mt * kTM);
-        const int n0 = nt * kTN;
+        const int row0 = __builtin_amdgcn_readfirstlane(a.groups.row0[g]) + mt * kBM;
+        const int rows_valid = min(kBM, grows - mt * kBM);
+        const int n0 = nt * kBN;
         const bool sh = (g == a.shared_group);
         const uint8_t *A = (const uint8_t *)(sh ? a.A_shared : a.A_routed) + (int64_t)row0 * K;
-        const float *As = (sh ? a.As_shared : a.As_routed) + row0;       // [K/128][ld]
-        const int s_ld = sh ? lds_rows_shared : lds_rows_routed;
+        const float *As = (sh ? a.As_shared : a.As_routed) + row0;      // [K/128][ld]
         const uint8_t *B = (const uint8_t *)a.B + ((int64_t)g * N + n0) * K;
-        const __amdgpu_buffer_rsrc_t ra = rsrc8(A, (int64_t)rows_valid * K);
-        const __amdgpu_buffer_rsrc_t rb = rsrc8(B, (int64_t)min(kTN, N - n0) * K);
-        const __amdgpu_buffer_rsrc_t rs = rsrc8(As, ((int64_t)(KT - 1) * s_ld + rows_valid) * 4);
-        // weight block scales: gate/up packed per 32 rows, down per 128 rows
-        const int kb = K / 128;
-        const float *Bs = a.Bs + (int64_t)g * (SWIGLU ? (N / 32) : (N / 128)) * kb;
-
-        f32x16 acc[2][4];
+        Tile8 t;
+        t.KT = K / kGrpB;
+        t.s_ld = sh ? lds_rows_shared : lds_rows_routed;
+        t.ncb = min(kBN, N - n0) / 16;
+        t.cbstride = t.KT * 2048;
+        t.ra = rsrc8(A, (int64_t)rows_valid * K);
+        t.rb = rsrc8(B, (int64_t)t.ncb * t.cbstride);
+        t.rs = rsrc8(As, ((int64_t)(t.KT - 1) * t.s_ld + rows_valid) * 4);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = (f32x16){};
-
-        auto issue = [&](int kt, int buf) {
-            const int soff = kt * kBK8;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) rows_to_lds(ra, lds_a[buf], wave * 8 + i, voff_even, voff_odd, K, soff);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) rows_to_lds(rb, lds_b[buf], wave * 4 + i, voff_even, voff_odd, K, soff);
-            // 256 scales = 64 lanes x 16 bytes, contiguous.  The step offset is
-            // in the range-checked vector offset, so on the last step the
-            // scales of rows past the group read as zero instead of past the
-            // end of the scale array.
-            if (wave == 0)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)lds_s[buf], 16,
-                                                         kt * s_ld * 4 + lane * 16, 0, 0, 0);
-        };
-
-        auto step = [&](int kt, int buf) {
-            const uint8_t *Al = lds_a[buf];
-            const uint8_t *Bl = lds_b[buf];
-            // weight scales of this step for the 4 column blocks (wave-uniform)
-            float sb[4];
-#pragma unroll
-            for (int nb = 0; nb < 4; ++nb) {
-                const int n = n0 + nb * 32;
-                const int nblk = SWIGLU ? (n >> 5) : (n >> 7);
-                sb[nb] = (n < N) ? Bs[nblk * kb + kt] : 0.0f;
-            }
-            i32x8 bf[4][2];
-#pragma unroll
-            for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-                for (int kk = 0; kk < 2; ++kk) {
-                    const int c = kk * 4 + rd_hi * 2;
-                    const i32x4 lo = *(const i32x4 *)&Bl[b_rd + nb * 32 * kRowB + (((c) ^ swz) << 4)];
-                    const i32x4 hi = *(const i32x4 *)&Bl[b_rd + nb * 32 * kRowB + (((c + 1) ^ swz) << 4)];
-                    bf[nb][kk] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                }
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
-                i32x8 af[2];
-#pragma unroll
-                for (int kk = 0; kk < 2; ++kk) {
-                    const int c = kk * 4 + rd_hi * 2;
-                    const i32x4 lo = *(const i32x4 *)&Al[a_rd + mb * 32 * kRowB + (((c) ^ swz) << 4)];
-                    const i32x4 hi = *(const i32x4 *)&Al[a_rd + mb * 32 * kRowB + (((c + 1) ^ swz) << 4)];
-                    af[kk] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                }
-                // row scales of the 16 accumulator rows of this lane
-                float sa[16];
-                const int rbase = wave * 64 + mb * 32 + rd_hi * 4;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const f32x4 v = *(const f32x4 *)&lds_s[buf][rbase + j * 8];
-                    sa[4 * j + 0] = v[0];
-                    sa[4 * j + 1] = v[1];
-                    sa[4 * j + 2] = v[2];
-                    sa[4 * j + 3] = v[3];
-                }
-#pragma unroll
-                for (int nb = 0; nb < 4; ++nb) {
-                    f32x16 t = (f32x16){};
-                    t = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[0], bf[nb][0], t, 0, 0, 0, 127, 0, 127);
-                    t = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af[1], bf[nb][1], t, 0, 0, 0, 127, 0, 127);
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) acc[mb][nb][r] += t[r] * (sa[r] * sb[nb]);
-                }
-            }
-        };
-
-        issue(0, 0);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        for (int kt = 0; kt < KT; kt += 2) {     // K/128 is even or odd: guard the second half
-            if (kt + 1 < KT) issue(kt + 1, 1);
-            __builtin_amdgcn_sched_barrier(0);
-            step(kt, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
-            if (kt + 1 >= KT) break;
-            if (kt + 2 < KT) issue(kt + 2, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            step(kt + 1, 1);
-            __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
+        for (int i = 0; i < 4; ++i) {
+            const int r = frow + 8 * i;
+            t.va[i] = r < rows_valid ? r * K + ((i & 1) ? fch_odd : fch_even) : (int)0x80000000u;
+        }
+        if constexpr (SWIGLU) {
+            // [G][f/128][gate, up][K/128]: tile nt covers gate/up scale block nt
+            const int f = N / 2;
+            t.sbp = a.Bs + (((int64_t)g * (f / 128) + nt) * 2 + (wn & 1)) * t.KT;
+        } else {
+            // [G][N/128][K/128]: wave columns n0 + 64 wn .. + 63
+            const int nb = min(2 * nt + (wn >> 1), N / 128 - 1);
+            t.sbp = a.Bs + ((int64_t)g * (N / 128) + nb) * t.KT;
         }
 
-        // Epilogue (bf16 out), register r of a 32x32 block = row 8 (r/4) + 4 (lane/32) + r%4.
-        bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
+        f32x4 acc[8][4];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = (f32x4){};
+
+        float sb_next = t.sbp[0];
+        __builtin_amdgcn_sched_barrier(0);
+        fill8(t, ring[0], w.wave, lane, 0);
+        for (int kg = 0; kg < t.KT; kg += 2) {
+            kgroup8<0>(t, w, ring, acc, sb_next, kg);
+            if (kg + 1 < t.KT) kgroup8<1>(t, w, ring, acc, sb_next, kg + 1);
+        }
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // the clamped fill issued by the last group
+        __syncthreads();                                     // ring idle in every wave
+
+        // Accumulator register i of a 16x16 block holds row 4 (lane / 16) + i
+        // and column lane % 16.
         if constexpr (SWIGLU) {
             const int f = N / 2;
-            const int f0 = nt * (kTN / 2) + (lane & 31);
+            const int s_ld = t.s_ld;
+            uint8_t *H = (uint8_t *)(sh ? a.C_shared : a.C_routed);
+            float *Hs = (sh ? a.Cs_shared : a.Cs_routed) + (int64_t)nt * s_ld + row0;
+            // wave pair p (same rows, same h columns): wn = 2 q (gate) and 2 q + 1 (up)
+            const int q = wn >> 1;
+            const int p = wm * 2 + q;
+            float *xch = (float *)(p == 0 ? lds_a0 : p == 1 ? lds_b0 : p == 2 ? lds_a1 : lds_b1);
+            if (wn & 1) {
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
+                for (int rb = 0; rb < 8; ++rb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int lr = wave * 64 + mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
-                    if (lr < rows_valid) {
-                        bf16 *dst = C + (int64_t)(row0 + lr) * f + f0;
+                    for (int cb = 0; cb < 4; ++cb)
+                        *(f32x4 *)&xch[((rb * 4 + cb) * 64 + lane) * 4] = acc[rb][cb];
+            }
+            __syncthreads();
+            if (!(wn & 1)) {
+                // h in bf16 (kept in acc), then this wave's maximum of |h| over
+                // its 64 channels of each row, stored for the partner wave
+                float *mx = q ? lds_s1 : lds_s0;
 #pragma unroll
-                        for (int p = 0; p < 2; ++p) {
-                            const float gt = acc[mb][2 * p][r];
-                            const float up = acc[mb][2 * p + 1][r];
-                            dst[p * 32] = f2bf(gt / (1.0f + __expf(-gt)) * up);
+                for (int rb = 0; rb < 8; ++rb) {
+                    f32x4 am = (f32x4){};
+#pragma unroll
+                    for (int cb = 0; cb < 4; ++cb) {
+                        const f32x4 up = *(const f32x4 *)&xch[((rb * 4 + cb) * 64 + lane) * 4];
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float gt = acc[rb][cb][i];
+                            const float hv = bf2f(f2bf(gt / (1.0f + __expf(-gt)) * up[i]));
+                            acc[rb][cb][i] = hv;
+                            am[i] = fmaxf(am[i], fabsf(hv));
                         }
                     }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+                        for (int m = 1; m < 16; m <<= 1) am[i] = fmaxf(am[i], __shfl_xor(am[i], m, 16));
+                    }
+                    if ((lane & 15) == 0) *(f32x4 *)&mx[w.s_rd + rb * 16] = am;
                 }
+            }
+            __syncthreads();
+            uint8_t *stg = lds_a0;   // [256 rows][128 codes]; the up values were read above
+            if (!(wn & 1)) {
+                const int col = q * 64 + (lane & 15);
+#pragma unroll
+                for (int rb = 0; rb < 8; ++rb) {
+                    const f32x4 m0 = *(const f32x4 *)&lds_s0[w.s_rd + rb * 16];
+                    const f32x4 m1 = *(const f32x4 *)&lds_s1[w.s_rd + rb * 16];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float am = fmaxf(m0[i], m1[i]);
+                        const float s = am > 0.0f ? am / 448.0f : 1.0f;   // IEEE division
+                        const int row = wm * 128 + rb * 16 + 4 * (lane >> 4) + i;
+                        const uint32_t c4 = e4m3_pack4(acc[rb][0][i] / s, acc[rb][1][i] / s,
+                                                       acc[rb][2][i] / s, acc[rb][3][i] / s);
+#pragma unroll
+                        for (int cb = 0; cb < 4; ++cb)
+                            stg[row * kGrpB + col + cb * 16] = (uint8_t)(c4 >> (8 * cb));
+                        if (q == 0 && (lane & 15) == 0 && row < rows_valid) Hs[row] = s;
+                    }
+                }
+            }
+            __syncthreads();
+            for (int c = tid; c < kBM * (kGrpB / 16); c += kThreads8) {
+                const int row = c >> 3, ch = c & 7;
+                if (row < rows_valid)
+                    *(uint4 *)&H[(int64_t)(row0 + row) * f + nt * 128 + ch * 16] =
+                        *(const uint4 *)&stg[row * kGrpB + ch * 16];
+            }
+            __syncthreads();   // the staging area is the next tile's first stage
         } else {
-            const int c0 = n0 + (lane & 31);
+            bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
+            const int col0 = n0 + wn * 64 + (lane & 15);
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
+            for (int rb = 0; rb < 8; ++rb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int lr = wave * 64 + mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
-                    if (lr < rows_valid) {
-                        bf16 *dst = C + (int64_t)(row0 + lr) * N;
+                for (int i = 0; i < 4; ++i) {
+                    const int row = wm * 128 + rb * 16 + 4 * (lane >> 4) + i;
+                    if (row < rows_valid) {
+                        bf16 *dst = C + (int64_t)(row0 + row) * N;
 #pragma unroll
-                        for (int nb = 0; nb < 4; ++nb) {
-                            const int col = c0 + nb * 32;
-                            if (col < N) dst[col] = f2bf(acc[mb][nb][r]);
+                        for (int cb = 0; cb < 4; ++cb) {
+                            const int col = col0 + cb * 16;
+                            if (col < N) dst[col] = f2bf(acc[rb][cb][i]);
                         }
                     }
                 }
@@ -255,8 +359,8 @@ hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int mt_max, int num_c
                            int32_t lds_rows_routed, int32_t lds_rows_shared, hipStream_t s)
 {
     if (mt_max <= 0) return hipSuccess;
-    if (a.K % 128) return hipErrorNotSupported;
-    const int64_t tiles = (int64_t)mt_max * ((a.N + kTN - 1) / kTN);
+    if (a.K % 128 || a.N % 128 || (swiglu && a.N % 256)) return hipErrorNotSupported;
+    const int64_t tiles = (int64_t)mt_max * ((a.N + kBN - 1) / kBN);
     int grid = num_cus < tiles ? num_cus : (int)tiles;
     if (grid >= 8) grid &= ~7;
     if (swiglu)

@@ -96,24 +96,26 @@ hipError_t launch_quantize_fp8(const void *x, int32_t n_rows, const int32_t *n_r
                                int32_t d, void *xq, float *xs, int32_t scale_ld, int num_cus,
                                hipStream_t s);
 
-// Weight packing at create time.
-// Interleaves gate and up rows in blocks of `interleave` rows: packed row
-// 2*il*b + i is gate row il*b + i for i < il and up row il*b + (i - il)
-// otherwise.  bf16 uses il = 16 (a 32-column MFMA block then holds matching
-// gate and up columns), fp8 uses il = 32.  elem_bytes is 2 (bf16) or 1 (e4m3).
+// Weight packing at create time.  Gate and up rows are interleaved in
+// blocks of `interleave` rows: packed row 2*il*b + i is gate row il*b + i for
+// i < il and up row il*b + (i - il) otherwise.  bf16 uses il = 16 (a 32-column
+// MFMA block then holds matching gate and up columns); fp8 uses il = 64 (each
+// wave's 64 columns are all gate or all up rows of one 128-row scale block).
 constexpr int kInterleaveBf16 = 16;
-constexpr int kInterleaveFp8 = 32;
-hipError_t launch_pack_gate_up(const void *gate, const void *up, void *packed, int32_t n_mats,
-                               int32_t f, int32_t d, int32_t elem_bytes, int32_t interleave,
-                               hipStream_t s);
+constexpr int kInterleaveFp8 = 64;
 // bf16 weights in MFMA fragment order (the layout both bf16 grouped-GEMM
 // kernels read B in): chunk ((m * N/32 + n/32) * K/16 + k/16) * 64 + n % 32 +
 // 32 ((k/8) % 2) of 16 bytes holds row n, columns k..k+7 (k % 8 == 0).  With
 // `up` non-null the packed rows interleave gate and up by `interleave`.
 hipError_t launch_pack_frag_bf16(const void *gate, const void *up, void *dst, int32_t n_mats,
                                  int32_t N, int32_t K, int32_t interleave, hipStream_t s);
-// Per-32-row scales of the packed matrix from the 128x128 block scales:
-// packed_s[m][p32][kb] = (gate or up)_s[m][(32*b)/128][kb].
+// e4m3 weights in the fragment order of the 16x16x128 f8 MFMA: chunk
+// ((m * N/16 + n/16) * K/128 + k/128) * 128 + 64 ((k/16) % 2) + n % 16 +
+// 16 ((k % 128) / 32) of 16 bytes holds row n, bytes k..k+15 (k % 16 == 0).
+hipError_t launch_pack_frag_fp8(const void *gate, const void *up, void *dst, int32_t n_mats,
+                                int32_t N, int32_t K, int32_t interleave, hipStream_t s);
+// Gate/up block scales of the fp8 path, [m][f/128][gate, up][d/128], from the
+// two [m][f/128][d/128] arrays.
 hipError_t launch_pack_gate_up_scales(const float *gs, const float *us, float *packed_s,
                                       int32_t n_mats, int32_t f, int32_t d, hipStream_t s);
 

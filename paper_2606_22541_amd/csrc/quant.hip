@@ -4,19 +4,6 @@
 
 namespace moe {
 
-// e4m3 (OCP E4M3FN) code of v, round to nearest even.  |v| is clamped to 448
-// first, which makes the conversion saturating.
-__device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float d)
-{
-    a = fminf(fmaxf(a, -448.0f), 448.0f);
-    b = fminf(fmaxf(b, -448.0f), 448.0f);
-    c = fminf(fmaxf(c, -448.0f), 448.0f);
-    d = fminf(fmaxf(d, -448.0f), 448.0f);
-    int v = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
-    v = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, v, true);
-    return (uint32_t)v;
-}
-
 // One group of 128 channels is handled by 16 lanes, 8 channels each.
 __global__ __launch_bounds__(256)
 void k_quantize_fp8(const uint4 *__restrict__ x, int32_t n_rows, const int32_t *__restrict__ n_rows_dev,
@@ -70,49 +57,26 @@ hipError_t launch_quantize_fp8(const void *x, int32_t n_rows, const int32_t *n_r
 // ---------------------------------------------------------------------------
 // Weight packing (create time only).
 // ---------------------------------------------------------------------------
-__global__ void k_pack_gate_up(const uint4 *__restrict__ gate, const uint4 *__restrict__ up,
-                               uint4 *__restrict__ packed, int32_t n_mats, int32_t f,
-                               int32_t row_vecs, int32_t il)
-{
-    const int64_t total = (int64_t)n_mats * 2 * f * row_vecs;
-    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
-         q += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t prow = q / row_vecs;
-        const int c = (int)(q - prow * row_vecs);
-        const int m = (int)(prow / (2 * f));
-        const int p = (int)(prow - (int64_t)m * 2 * f);
-        const int b = p / (2 * il), i = p % (2 * il);
-        const int src_row = b * il + (i % il);
-        const uint4 *src = (i < il) ? gate : up;
-        packed[q] = src[((int64_t)m * f + src_row) * row_vecs + c];
-    }
-}
-
-hipError_t launch_pack_gate_up(const void *gate, const void *up, void *packed, int32_t n_mats,
-                               int32_t f, int32_t d, int32_t elem_bytes, int32_t interleave,
-                               hipStream_t s)
-{
-    const int row_vecs = d * elem_bytes / 16;
-    hipLaunchKernelGGL(k_pack_gate_up, dim3(4096), dim3(256), 0, s, (const uint4 *)gate,
-                       (const uint4 *)up, (uint4 *)packed, n_mats, f, row_vecs, interleave);
-    return hipGetLastError();
-}
-
+// Gate/up weight scales of the fp8 path: [m][f/128][gate, up][d/128], so
+// that a 256-column tile of the packed matrix (gate and up rows
+// [128 t, 128 t + 128), interleaved by 64) finds both of its scale rows
+// next to each other.
 __global__ void k_pack_gate_up_scales(const float *__restrict__ gs, const float *__restrict__ us,
                                       float *__restrict__ ps, int32_t n_mats, int32_t f,
                                       int32_t kblocks)
 {
-    const int p32n = 2 * f / 32;
-    const int64_t total = (int64_t)n_mats * p32n * kblocks;
+    const int fb_n = f / 128;
+    const int64_t total = (int64_t)n_mats * fb_n * 2 * kblocks;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
          q += (int64_t)gridDim.x * blockDim.x) {
         const int kb = (int)(q % kblocks);
-        const int64_t rest = q / kblocks;
-        const int p32 = (int)(rest % p32n);
-        const int m = (int)(rest / p32n);
-        const int fblk = ((p32 >> 1) * 32) / 128;
-        const float *src = (p32 & 1) ? us : gs;
-        ps[q] = src[((int64_t)m * (f / 128) + fblk) * kblocks + kb];
+        int64_t rest = q / kblocks;
+        const int u = (int)(rest & 1);
+        rest >>= 1;
+        const int fb = (int)(rest % fb_n);
+        const int m = (int)(rest / fb_n);
+        const float *src = u ? us : gs;
+        ps[q] = src[((int64_t)m * fb_n + fb) * kblocks + kb];
     }
 }
 
@@ -121,6 +85,52 @@ hipError_t launch_pack_gate_up_scales(const float *gs, const float *us, float *p
 {
     hipLaunchKernelGGL(k_pack_gate_up_scales, dim3(256), dim3(256), 0, s, gs, us, packed_s,
                        n_mats, f, d / 128);
+    return hipGetLastError();
+}
+
+// e4m3 weights in the fragment order of v_mfma_scale_f32_16x16x128_f8f6f4.
+// Row n (of N) and byte k (of K) of matrix m go to 16-byte chunk
+// ((m * N/16 + n/16) * K/128 + k/128) * 128 + 64 h + lane, byte k % 16, with
+// lane = n % 16 + 16 * ((k % 128) / 32) and h = (k / 16) % 2: a 16-column x
+// 128-K fragment is 2 KB of consecutive memory, two 1 KB halves of one
+// 16-byte chunk per lane, and lane l's 32 bytes are the K bytes
+// [32 (l / 16), 32 (l / 16) + 32) of the group for column l % 16 (the token
+// rows are read with the same K assignment).  With `up` given, packed row n
+// interleaves gate and up rows in blocks of `il` (N = 2 f rows per matrix).
+__global__ void k_pack_frag_fp8(const uint4 *__restrict__ gate, const uint4 *__restrict__ up,
+                                uint4 *__restrict__ dst, int32_t n_mats, int32_t N, int32_t K,
+                                int32_t il)
+{
+    const int64_t total = (int64_t)n_mats * N * (K / 16);
+    const int kgs = K / 128, nbs = N / 16, row_vecs = K / 16;
+    const int rows_per_src = up ? N / 2 : N;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int lane = (int)(q & 63);
+        const int h = (int)((q >> 6) & 1);
+        int64_t rest = q >> 7;
+        const int kg = (int)(rest % kgs);
+        rest /= kgs;
+        const int nb = (int)(rest % nbs);
+        const int m = (int)(rest / nbs);
+        const int n = nb * 16 + (lane & 15);
+        const int kv = kg * 8 + 2 * (lane >> 4) + h;       // 16-byte chunk along K
+        const uint4 *src = gate;
+        int srow = n;
+        if (up) {
+            const int b = n / (2 * il), i = n % (2 * il);
+            src = (i < il) ? gate : up;
+            srow = b * il + (i % il);
+        }
+        dst[q] = src[((int64_t)m * rows_per_src + srow) * row_vecs + kv];
+    }
+}
+
+hipError_t launch_pack_frag_fp8(const void *gate, const void *up, void *dst, int32_t n_mats,
+                                int32_t N, int32_t K, int32_t interleave, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_pack_frag_fp8, dim3(4096), dim3(256), 0, s, (const uint4 *)gate,
+                       (const uint4 *)up, (uint4 *)dst, n_mats, N, K, interleave);
     return hipGetLastError();
 }
 

@@ -32,8 +32,6 @@ struct SlotWs {
     void *h_sh = nullptr;
     float *h_sh_s = nullptr;
     void *y_sh = nullptr;
-    void *h_bf = nullptr;        // fp8 mode: SiLU*up rows in bf16 before quantisation
-    void *h_sh_bf = nullptr;
     float *xsh_s = nullptr;      // fp8 mode with shared expert: x scales, transposed
     hipEvent_t ev = nullptr;
     bool ev_recorded = false;
@@ -83,7 +81,7 @@ Sizes sizes_of(const moe_stage_desc *d)
     if (s.nb_max < 1) s.nb_max = 1;
     s.w1 = align256(s.G * 2 * F * D * s.eb);
     s.w2 = align256(s.G * D * F * s.eb);
-    s.s1 = fp8 ? align256(s.G * (2 * F / 32) * (D / 128) * 4) : 0;
+    s.s1 = fp8 ? align256(s.G * (2 * F / 128) * (D / 128) * 4) : 0;
     s.s2 = fp8 ? align256(s.G * (D / 128) * (F / 128) * 4) : 0;
     const int64_t cap1 = s.cap > 0 ? s.cap : 1;
     const int64_t T1 = T > 0 ? T : 1;
@@ -94,11 +92,10 @@ Sizes sizes_of(const moe_stage_desc *d)
     if (fp8) b += align256(cap1 * D) + align256(cap1 * (D / 128) * 4);   // X_perm (fp8 only)
     b += align256(cap1 * F * s.eb) + (fp8 ? align256(cap1 * (F / 128) * 4) : 0);
     b += align256(cap1 * D * 2);
-    if (fp8) b += align256(cap1 * F * 2);
     if (d->has_shared_expert) {
         b += align256(T1 * F * s.eb) + (fp8 ? align256(T1 * (F / 128) * 4) : 0);
         b += align256(T1 * D * 2);
-        if (fp8) b += align256(T1 * F * 2) + align256(T1 * (D / 128) * 4);
+        if (fp8) b += align256(T1 * (D / 128) * 4);
     }
     s.per_slot = b;
     return s;
@@ -255,24 +252,22 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
         release(st);
         return MOE_ENOMEM;
     }
-    // Pack the weights; the shared expert is group E_loc.  bf16: [gate|up]
-    // interleaved by 16 rows and down, both in MFMA fragment order.  fp8:
-    // [gate|up] interleaved by 32 rows (row-major), down as is.
+    // Pack the weights in MFMA fragment order; the shared expert is group
+    // E_loc.  [gate|up] is interleaved by 16 rows (bf16) or 64 rows (fp8).
     hipError_t e = hipSuccess;
     const int64_t w1_mat = 2 * F * D * z.eb, w2_mat = D * F * z.eb;
     if (fp8) {
-        e = launch_pack_gate_up(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)F, (int32_t)D,
-                                (int32_t)z.eb, kInterleaveFp8, st->own);
+        e = launch_pack_frag_fp8(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)(2 * F),
+                                 (int32_t)D, kInterleaveFp8, st->own);
         if (e == hipSuccess)
-            e = hipMemcpyAsync(st->w2, w->w_down, (size_t)(El * w2_mat), hipMemcpyDeviceToDevice,
-                               st->own);
+            e = launch_pack_frag_fp8(w->w_down, nullptr, st->w2, (int32_t)El, (int32_t)D,
+                                     (int32_t)F, 0, st->own);
         if (e == hipSuccess && desc->has_shared_expert) {
-            e = launch_pack_gate_up(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
-                                    (int32_t)F, (int32_t)D, (int32_t)z.eb, kInterleaveFp8,
-                                    st->own);
+            e = launch_pack_frag_fp8(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
+                                     (int32_t)(2 * F), (int32_t)D, kInterleaveFp8, st->own);
             if (e == hipSuccess)
-                e = hipMemcpyAsync((char *)st->w2 + El * w2_mat, w->sh_down, (size_t)w2_mat,
-                                   hipMemcpyDeviceToDevice, st->own);
+                e = launch_pack_frag_fp8(w->sh_down, nullptr, (char *)st->w2 + El * w2_mat, 1,
+                                         (int32_t)D, (int32_t)F, 0, st->own);
         }
     } else {
         e = launch_pack_frag_bf16(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)(2 * F),
@@ -289,7 +284,7 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
         }
     }
     if (e == hipSuccess && fp8) {
-        const int64_t s1_mat = (2 * F / 32) * (D / 128), s2_mat = (D / 128) * (F / 128);
+        const int64_t s1_mat = (2 * F / 128) * (D / 128), s2_mat = (D / 128) * (F / 128);
         e = launch_pack_gate_up_scales(w->s_gate, w->s_up, st->s1, (int32_t)El, (int32_t)F,
                                        (int32_t)D, st->own);
         if (e == hipSuccess)
@@ -326,12 +321,11 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
         if (ok && fp8) ok = alloc(st, &sl.x_perm, cap1 * D) &&
                             alloc(st, &sl.x_perm_s, cap1 * (D / 128) * 4) &&
                             alloc(st, &sl.h_s, cap1 * (F / 128) * 4);
-        if (ok && fp8) ok = alloc(st, &sl.h_bf, cap1 * F * 2);
         if (ok && desc->has_shared_expert) {
             ok = alloc(st, &sl.h_sh, T1 * F * z.eb) && alloc(st, &sl.y_sh, T1 * D * 2);
             if (ok && fp8)
                 ok = alloc(st, &sl.h_sh_s, T1 * (F / 128) * 4) &&
-                     alloc(st, &sl.h_sh_bf, T1 * F * 2) && alloc(st, &sl.xsh_s, T1 * (D / 128) * 4);
+                     alloc(st, &sl.xsh_s, T1 * (D / 128) * 4);
         }
         if (!ok) {
             release(st);
@@ -444,8 +438,10 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     g1.As_shared = sl.xsh_s;
     g1.B = st->w1;
     g1.Bs = st->s1;
-    g1.C_routed = fp8 ? sl.h_bf : sl.h;
-    g1.C_shared = fp8 ? sl.h_sh_bf : sl.h_sh;
+    g1.C_routed = sl.h;             // fp8: e4m3 codes, with their scales in Cs
+    g1.C_shared = sl.h_sh;
+    g1.Cs_routed = sl.h_s;
+    g1.Cs_shared = sl.h_sh_s;
     g1.N = 2 * d.d_ff;
     g1.K = d.d_model;
     g1.shared_group = d.has_shared_expert ? d.n_local_experts : -1;
@@ -456,6 +452,8 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     g2.A_index = nullptr;            // H rows are already grouped by expert
     g2.A_index_div = 0;
     g2.A_routed_rows = 0;
+    g2.Cs_routed = nullptr;          // the down product writes bf16 Y
+    g2.Cs_shared = nullptr;
     g2.A_routed = sl.h;
     g2.A_shared = sl.h_sh;
     g2.As_routed = sl.h_s;
@@ -481,15 +479,6 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
             e = launch_gemm_bf16_small(g1, true, gmax, st->num_cus, s);
             if (e == hipSuccess) e = launch_gemm_bf16(g1, true, mt, st->num_cus, s);
         }
-    }
-    if (e == hipSuccess && fp8) {
-        // quantise h per row and 128 channels (scales transposed for the down GEMM)
-        ProfScope ps(st, 5, s);
-        e = launch_quantize_fp8(sl.h_bf, (int32_t)max_rows, sl.offsets + d.n_local_experts,
-                                d.d_ff, sl.h, sl.h_s, cap, st->num_cus, s);
-        if (e == hipSuccess && d.has_shared_expert)
-            e = launch_quantize_fp8(sl.h_sh_bf, T, nullptr, d.d_ff, sl.h_sh, sl.h_sh_s, tmax,
-                                    st->num_cus, s);
     }
     if (e == hipSuccess) {
         ProfScope ps(st, 3, s);
