@@ -125,9 +125,11 @@ struct Wave8 {
 // next group, then 32 MFMAs with the promotion of each row block.
 // The weight scale of the next group is loaded before the fills, so that
 // waiting for it never waits for them.
-template <int S>
+// RB row blocks of 16 rows per wave.  GUARD: row blocks at or past nrb (past
+// the group's last row) are skipped (wave-uniform branches).
+template <int S, int RB, bool GUARD>
 __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ring8 (&ring)[2],
-                                        f32x4 (&acc)[8][4], float &sb_next, int kg)
+                                        f32x4 (&acc)[RB][4], float &sb_next, int kg, int nrb)
 {
     __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0): this group's fills landed
     __builtin_amdgcn_s_barrier();                        // ... in every wave; the other stage is idle
@@ -148,28 +150,37 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
         bfr[cb] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     }
 #pragma unroll
-    for (int rb = 0; rb < 8; ++rb) {
-        const i32x4 lo = *(const i32x4 *)&As[w.a_rd0 + rb * 16 * kGrpB];
-        const i32x4 hi = *(const i32x4 *)&As[w.a_rd1 + rb * 16 * kGrpB];
-        const i32x8 af = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        const f32x4 sa = *(const f32x4 *)&Ss[w.s_rd + rb * 16];
-        f32x4 tq[4];
+    for (int rb = 0; rb < RB; ++rb) {
+        if (!GUARD || rb < nrb) {
+            const i32x4 lo = *(const i32x4 *)&As[w.a_rd0 + rb * 16 * kGrpB];
+            const i32x4 hi = *(const i32x4 *)&As[w.a_rd1 + rb * 16 * kGrpB];
+            const i32x8 af = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            const f32x4 sa = *(const f32x4 *)&Ss[w.s_rd + rb * 16];
+            f32x4 tq[4];
 #pragma unroll
-        for (int cb = 0; cb < 4; ++cb)
-            tq[cb] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bfr[cb], (f32x4){}, 0, 0,
-                                                                      0, 127, 0, 127);
-        const f32x4 s = sa * sb;
+            for (int cb = 0; cb < 4; ++cb)
+                tq[cb] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bfr[cb], (f32x4){}, 0, 0,
+                                                                          0, 127, 0, 127);
+            const f32x4 s = sa * sb;
 #pragma unroll
-        for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = tq[cb] * s + acc[rb][cb];
+            for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = tq[cb] * s + acc[rb][cb];
+        }
     }
 }
 
 }  // namespace
 
-template <bool SWIGLU>
+// RB = 8: 256-row tiles over the groups of more than kSmallRows rows (every
+// group with large_all).  RB = 6: one 192-row tile per group of 1..kSmallRows
+// rows, with the row blocks past the group's end skipped.
+template <bool SWIGLU, int RB>
 __global__ __launch_bounds__(kThreads8, 1)
 void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
 {
+    constexpr bool kSmall = RB < 8;
+    constexpr int kWRows = 16 * RB;                     // rows per wave
+    constexpr int kTRows = 2 * kWRows;                  // rows per tile
+    static_assert(!kSmall || kTRows == kSmallRows, "small tiles hold a whole small group");
     __shared__ __attribute__((aligned(1024))) uint8_t lds_a0[kStage8];
     __shared__ __attribute__((aligned(1024))) uint8_t lds_b0[kStage8];
     __shared__ __attribute__((aligned(1024))) uint8_t lds_a1[kStage8];
@@ -186,7 +197,8 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
     const int wm = w.wave >> 2, wn = w.wave & 3;        // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
     const int NT = (N + kBN - 1) / kBN;
-    const int total = __builtin_amdgcn_readfirstlane(a.groups.mt_base[a.G] * NT);
+    const int32_t *tbase = kSmall ? a.groups.st_base : a.large_all ? a.groups.mt_base : a.groups.lt_base;
+    const int total = __builtin_amdgcn_readfirstlane(tbase[a.G] * NT);
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
 
@@ -195,10 +207,10 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
     // weight fragments hold the same K bytes for column l % 16).
     {
         const int r = lane & 15, swz = (r >> 1) & 7, c0 = 2 * (lane >> 4);
-        w.a_rd0 = (wm * 128 + r) * kGrpB + ((c0 ^ swz) << 4);
-        w.a_rd1 = (wm * 128 + r) * kGrpB + (((c0 + 1) ^ swz) << 4);
+        w.a_rd0 = (wm * kWRows + r) * kGrpB + ((c0 ^ swz) << 4);
+        w.a_rd1 = (wm * kWRows + r) * kGrpB + (((c0 + 1) ^ swz) << 4);
         w.b_rd = wn * 4 * 2048 + lane * 16;
-        w.s_rd = wm * 128 + 4 * (lane >> 4);
+        w.s_rd = wm * kWRows + 4 * (lane >> 4);
     }
     // token fills: lane l covers row 32 w + 8 i + l / 8, physical chunk l % 8;
     // ((row / 2) % 8) = (4 (i % 2) + l / 16) % 8
@@ -208,13 +220,26 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
 
     for (int L = first; L < total; L += P) {
         int g, mt, nt;
-        decode_tile8(L, a.groups.mt_base, a.G, NT, g, mt, nt);
+        if constexpr (kSmall) {
+            // tile L: j-th small group, column tile nt
+            const int j = L / NT;
+            nt = L - j * NT;
+            mt = 0;
+            int lo = 0, hi = a.G;               // largest g with st_base[g] <= j
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (tbase[mid] <= j) lo = mid; else hi = mid;
+            }
+            g = lo;
+        } else {
+            decode_tile8(L, tbase, a.G, NT, g, mt, nt);
+        }
         g = __builtin_amdgcn_readfirstlane(g);
         mt = __builtin_amdgcn_readfirstlane(mt);
         nt = __builtin_amdgcn_readfirstlane(nt);
         const int grows = __builtin_amdgcn_readfirstlane(a.groups.rows[g]);
         const int row0 = __builtin_amdgcn_readfirstlane(a.groups.row0[g]) + mt * kBM;
-        const int rows_valid = min(kBM, grows - mt * kBM);
+        const int rows_valid = min(kTRows, grows - mt * kBM);
         const int n0 = nt * kBN;
         const bool sh = (g == a.shared_group);
         const uint8_t *A = (const uint8_t *)(sh ? a.A_shared : a.A_routed) + (int64_t)row0 * K;
@@ -243,18 +268,20 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
             t.sbp = a.Bs + ((int64_t)g * (N / 128) + nb) * t.KT;
         }
 
-        f32x4 acc[8][4];
+        f32x4 acc[RB][4];
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < RB; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[i][j] = (f32x4){};
 
+        // 16-row blocks of this wave's rows that hold rows of the group
+        const int nrb = __builtin_amdgcn_readfirstlane(min(RB, max(0, rows_valid - wm * kWRows + 15) / 16));
         float sb_next = t.sbp[0];
         __builtin_amdgcn_sched_barrier(0);
         fill8(t, ring[0], w.wave, lane, 0);
         for (int kg = 0; kg < t.KT; kg += 2) {
-            kgroup8<0>(t, w, ring, acc, sb_next, kg);
-            if (kg + 1 < t.KT) kgroup8<1>(t, w, ring, acc, sb_next, kg + 1);
+            kgroup8<0, RB, kSmall>(t, w, ring, acc, sb_next, kg, nrb);
+            if (kg + 1 < t.KT) kgroup8<1, RB, kSmall>(t, w, ring, acc, sb_next, kg + 1, nrb);
         }
         __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // the clamped fill issued by the last group
         __syncthreads();                                     // ring idle in every wave
@@ -272,7 +299,7 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
             float *xch = (float *)(p == 0 ? lds_a0 : p == 1 ? lds_b0 : p == 2 ? lds_a1 : lds_b1);
             if (wn & 1) {
 #pragma unroll
-                for (int rb = 0; rb < 8; ++rb)
+                for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
                     for (int cb = 0; cb < 4; ++cb)
                         *(f32x4 *)&xch[((rb * 4 + cb) * 64 + lane) * 4] = acc[rb][cb];
@@ -283,7 +310,7 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
                 // its 64 channels of each row, stored for the partner wave
                 float *mx = q ? lds_s1 : lds_s0;
 #pragma unroll
-                for (int rb = 0; rb < 8; ++rb) {
+                for (int rb = 0; rb < RB; ++rb) {
                     f32x4 am = (f32x4){};
 #pragma unroll
                     for (int cb = 0; cb < 4; ++cb) {
@@ -309,14 +336,14 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
             if (!(wn & 1)) {
                 const int col = q * 64 + (lane & 15);
 #pragma unroll
-                for (int rb = 0; rb < 8; ++rb) {
+                for (int rb = 0; rb < RB; ++rb) {
                     const f32x4 m0 = *(const f32x4 *)&lds_s0[w.s_rd + rb * 16];
                     const f32x4 m1 = *(const f32x4 *)&lds_s1[w.s_rd + rb * 16];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const float am = fmaxf(m0[i], m1[i]);
                         const float s = am > 0.0f ? am / 448.0f : 1.0f;   // IEEE division
-                        const int row = wm * 128 + rb * 16 + 4 * (lane >> 4) + i;
+                        const int row = wm * kWRows + rb * 16 + 4 * (lane >> 4) + i;
                         const uint32_t c4 = e4m3_pack4(acc[rb][0][i] / s, acc[rb][1][i] / s,
                                                        acc[rb][2][i] / s, acc[rb][3][i] / s);
 #pragma unroll
@@ -338,10 +365,10 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
             bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
             const int col0 = n0 + wn * 64 + (lane & 15);
 #pragma unroll
-            for (int rb = 0; rb < 8; ++rb)
+            for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int row = wm * 128 + rb * 16 + 4 * (lane >> 4) + i;
+                    const int row = wm * kWRows + rb * 16 + 4 * (lane >> 4) + i;
                     if (row < rows_valid) {
                         bf16 *dst = C + (int64_t)(row0 + row) * N;
 #pragma unroll
@@ -355,20 +382,35 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
     }
 }
 
-hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int mt_max, int num_cus,
+hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int mt_max, int g_max, int num_cus,
                            int32_t lds_rows_routed, int32_t lds_rows_shared, hipStream_t s)
 {
     if (mt_max <= 0) return hipSuccess;
     if (a.K % 128 || a.N % 128 || (swiglu && a.N % 256)) return hipErrorNotSupported;
-    const int64_t tiles = (int64_t)mt_max * ((a.N + kBN - 1) / kBN);
-    int grid = num_cus < tiles ? num_cus : (int)tiles;
-    if (grid >= 8) grid &= ~7;
+    const int64_t NT = (a.N + kBN - 1) / kBN;
+    auto grid_for = [&](int64_t tiles) {
+        int grid = num_cus < tiles ? num_cus : (int)tiles;
+        if (grid >= 8) grid &= ~7;
+        return grid;
+    };
+    // groups of 1..kSmallRows rows (one 192-row tile each), then the others
+    // (either launch may find no tiles)
+    if (!a.large_all && g_max > 0) {
+        const int grid = grid_for((int64_t)g_max * NT);
+        if (swiglu)
+            hipLaunchKernelGGL((k_gemm_fp8<true, 6>), dim3(grid), dim3(kThreads8), 0, s, a,
+                               lds_rows_routed, lds_rows_shared);
+        else
+            hipLaunchKernelGGL((k_gemm_fp8<false, 6>), dim3(grid), dim3(kThreads8), 0, s, a,
+                               lds_rows_routed, lds_rows_shared);
+    }
+    const int grid = grid_for((int64_t)mt_max * NT);
     if (swiglu)
-        hipLaunchKernelGGL(k_gemm_fp8<true>, dim3(grid), dim3(kThreads8), 0, s, a, lds_rows_routed,
-                           lds_rows_shared);
+        hipLaunchKernelGGL((k_gemm_fp8<true, 8>), dim3(grid), dim3(kThreads8), 0, s, a,
+                           lds_rows_routed, lds_rows_shared);
     else
-        hipLaunchKernelGGL(k_gemm_fp8<false>, dim3(grid), dim3(kThreads8), 0, s, a, lds_rows_routed,
-                           lds_rows_shared);
+        hipLaunchKernelGGL((k_gemm_fp8<false, 8>), dim3(grid), dim3(kThreads8), 0, s, a,
+                           lds_rows_routed, lds_rows_shared);
     return hipGetLastError();
 }
 

@@ -75,7 +75,12 @@ hipError_t launch_gemm_bf16_small(const GemmArgs &a, bool swiglu, int g_max, int
 
 // e4m3 grouped GEMM with 128-block scales (same conventions; the A scales
 // are transposed, [K/128][ld] with ld = lds_rows_routed / lds_rows_shared).
-hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int mt_max, int num_cus,
+// swiglu = true writes e4m3 h with one scale per row and 128 channels
+// (C and Cs, the scales transposed like the A scales).  Groups of
+// 1..kSmallRows rows run as one 192-row tile each (g_max bounds the group
+// count), the others as 256-row tiles (mt_max bounds those); with
+// large_all every group takes 256-row tiles.
+hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int mt_max, int g_max, int num_cus,
                            int32_t lds_rows_routed, int32_t lds_rows_shared, hipStream_t s);
 
 struct CombineArgs {

@@ -474,7 +474,7 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     {
         ProfScope ps(st, 2, s);
         if (fp8) {
-            e = launch_gemm_fp8(g1, true, mt, st->num_cus, cap, tmax, s);
+            e = launch_gemm_fp8(g1, true, mt, gmax, st->num_cus, cap, tmax, s);
         } else {
             e = launch_gemm_bf16_small(g1, true, gmax, st->num_cus, s);
             if (e == hipSuccess) e = launch_gemm_bf16(g1, true, mt, st->num_cus, s);
@@ -483,7 +483,7 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     if (e == hipSuccess) {
         ProfScope ps(st, 3, s);
         if (fp8) {
-            e = launch_gemm_fp8(g2, false, mt, st->num_cus, cap, tmax, s);
+            e = launch_gemm_fp8(g2, false, mt, gmax, st->num_cus, cap, tmax, s);
         } else {
             // the down product (K = f) keeps 256x256 tiles for every group:
             // at ~130 rows its 28 column tiles per expert already fill the GPU

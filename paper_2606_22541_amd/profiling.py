@@ -44,8 +44,8 @@ NAME_MAP = (
     ("void moe::k_gemm_bf16_small<true>", "gemm_gate_up_swiglu"),
     ("void moe::k_gemm_bf16<true>", "gemm_gate_up_swiglu"),
     ("void moe::k_gemm_bf16<false>", "gemm_down"),
-    ("void moe::k_gemm_fp8<true>", "gemm_gate_up_swiglu_fp8"),
-    ("void moe::k_gemm_fp8<false>", "gemm_down_fp8"),
+    ("void moe::k_gemm_fp8<true,", "gemm_gate_up_swiglu_fp8"),
+    ("void moe::k_gemm_fp8<false,", "gemm_down_fp8"),
     ("moe::k_combine", "combine"),
     ("void moe::k_gather", "gather"),
     ("moe::k_hist", "dispatch_index"),
