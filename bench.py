@@ -41,7 +41,9 @@ def gemm_accounting(cfg, counts_local, T):
     """Algorithmic FLOPs and HBM bytes of one launch of each grouped GEMM.
 
     gate/up: 4 d f FLOP per row; reads each active expert's [2f, d] weights
-    once, the routed rows of X_perm (and x for the shared expert), writes H.
+    once and every routed row once (bf16: the token row of x, found through
+    slot_of_row; fp8: the row of X_perm), and the shared expert's rows of x;
+    writes H.
     down:    2 d f FLOP per row; reads [d, f] weights, H; writes Y.
     """
     d, f = cfg.d, cfg.f
@@ -254,6 +256,73 @@ def describe(r):
         per=r["n_local_slots"] // c.E_loc)
 
 
+def run_layers(n_layers, passes=3):
+    """Layer-oblivious submission against host-in-the-loop dispatch, on one
+    stage holding n_layers copies of the c1 expert share (7168 x 2048, 8
+    local experts).  One pass submits one c1 micro-batch per layer, layers in
+    a fixed shuffled order, each naming its layer through a device int32.
+      device-resolved: every pass is enqueued ahead; the GEMM kernels pick the
+        layer's weights from the on-device address table (no host in the loop);
+      host-dispatched: before each layer the host learns which layer comes
+        next by reading the id back from the device (which waits for the
+        stream), then enqueues it -- the dispatch pattern whose per-layer
+        latency the super kernel removes.
+    Returns ms per layer for both and their difference (the per-layer host
+    dispatch bubble)."""
+    import torch
+    from paper_2606_22541_amd import inputs
+    from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
+
+    cfg = inputs.CONFIGS["c1"]
+    w = inputs.make_weights(cfg, "cuda")
+    mb = inputs.make_microbatches(cfg, "cuda")[0]
+    T = mb.ids.shape[0]
+    stage = ExpertStage(cfg, [w] * n_layers, n_slots=2, max_tokens=T)   # n_layers packed copies
+    del w
+    ids, wt = to_device_routing(mb.ids, mb.w)
+    x = mb.x.clone()
+    outs = [torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+    order = [int(l) for l in np.random.default_rng(0).permutation(n_layers)]
+    lids = [torch.tensor([l], dtype=torch.int32, device="cuda") for l in order]
+    mbs = [stage.microbatch(x, ids, wt, outs[i % 2], layer_id=lids[i]) for i in range(n_layers)]
+    main = torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    def device_resolved():
+        for m in mbs:
+            stage.submit(m, main)
+
+    def host_dispatched():
+        for i, m in enumerate(mbs):
+            with torch.cuda.stream(main):
+                assert int(lids[i].item()) == order[i]   # synchronising read of the layer id
+            stage.submit(m, main)
+
+    res = {}
+    for name, fn in (("device_resolved", device_resolved), ("host_dispatched", host_dispatched)):
+        fn()                                           # warm-up pass
+        stage.sync()
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record(main)
+        for _ in range(passes):
+            fn()
+        end.record(main)
+        stage.sync()
+        torch.cuda.synchronize()
+        res[name] = start.elapsed_time(end) / (passes * n_layers)
+    stage.close()
+    return {
+        "layers": n_layers,
+        "workload": "c1 expert share (T=4096, d=7168, f=2048, 8 of 256 experts local, top-8, "
+                    "bf16) x %d layers resident, layers in shuffled order" % n_layers,
+        "ms_per_layer_device_resolved": round(res["device_resolved"], 4),
+        "ms_per_layer_host_dispatched": round(res["host_dispatched"], 4),
+        "host_bubble_us_per_layer": round((res["host_dispatched"] - res["device_resolved"]) * 1e3, 1),
+    }
+
+
 def cpu_baseline(name="c1", min_seconds=10.0):
     """The CPU oracle on the full T=4096 micro-batch of the primary workload."""
     import oracle
@@ -296,6 +365,8 @@ def main():
     ap.add_argument("--secondary", default="c1p,c3,c2,c4",
                     help="comma-separated further workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=8,
+                    help="layers for the layer-oblivious dispatch measurement (0: skip)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -353,6 +424,9 @@ def main():
             "kernels": stream_rooflines(sec),
         }
         _log("[bench] %s done" % name)
+    if args.layers > 0:
+        line["layer_oblivious"] = run_layers(args.layers)
+        _log("[bench] layer-oblivious dispatch done")
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload)
         _log("[bench] cpu baseline done")

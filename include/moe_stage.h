@@ -17,6 +17,12 @@
  *      token), and
  *   4. does all of it on the caller's stream per micro-batch, without any
  *      device-wide barrier or host read-back (sections 3.4.1 and 3.4.2).
+ * A stage may hold the expert weights of several layers (the MoE Super
+ * Kernel of section 3.4.2: weights of all L layers resident, an on-device
+ * table of their addresses, the layer id a device-side argument): a
+ * micro-batch then names its layer through a device pointer that the GEMM
+ * kernels read when they run, so work for any layer can be enqueued ahead
+ * of time without the host knowing which layer it is.
  *
  * Conventions (section 3.2: buffers are allocated once at initialisation and
  * live as long as the framework; weights stay resident in HBM):
@@ -77,6 +83,7 @@ typedef int32_t moe_status;
 #define MOE_EBADID         (-4)   /* device saw an expert id outside [-1, n_experts) */
 #define MOE_EUNSUPPORTED   (-5)   /* shape or mode this build does not support */
 #define MOE_EBUSY          (-6)   /* slot still in flight (non-blocking query) */
+#define MOE_EBADLAYER      (-7)   /* device saw a layer id outside [0, n_layers) */
 
 enum { MOE_DTYPE_BF16 = 0, MOE_DTYPE_FP8_E4M3_B128 = 1 };
 enum { MOE_COMBINE_OVERWRITE = 0, MOE_COMBINE_ACCUMULATE = 1 };
@@ -84,7 +91,8 @@ enum { MOE_COMBINE_OVERWRITE = 0, MOE_COMBINE_ACCUMULATE = 1 };
 /* Stage shape.  Requirements: d_model and d_ff multiples of 128;
  * 1 <= n_experts <= 1024; 0 <= first_local_expert;
  * 1 <= n_local_experts <= 256; first_local_expert + n_local_experts <=
- * n_experts; 1 <= top_k <= 32; 0 <= max_tokens; 1 <= n_slots <= 64. */
+ * n_experts; 1 <= top_k <= 32; 0 <= max_tokens; 1 <= n_slots <= 64;
+ * 1 <= n_layers <= 1024 (every layer has the same shape and local experts). */
 typedef struct {
     int32_t d_model;             /* hidden size d (paper: H) */
     int32_t d_ff;                /* expert intermediate size f */
@@ -96,9 +104,11 @@ typedef struct {
     int32_t n_slots;             /* micro-batches that may be in flight at once */
     int32_t dtype;               /* MOE_DTYPE_* */
     int32_t has_shared_expert;   /* 1: one always-on shared SwiGLU expert */
+    int32_t n_layers;            /* layers whose weights the stage holds (paper: L) */
 } moe_stage_desc;
 
-/* Expert weights (device pointers; read during create only).
+/* Expert weights of one layer (device pointers; read during create only;
+ * moe_stage_create takes an array of n_layers of them, layer 0 first).
  * bf16:  w_gate, w_up [E_loc][f][d] bf16; w_down [E_loc][d][f] bf16.
  * fp8:   the same shapes as e4m3 bytes, with fp32 scales per 128x128 block:
  *        s_gate, s_up [E_loc][f/128][d/128], s_down [E_loc][d/128][f/128].
@@ -115,7 +125,13 @@ typedef struct {
  * x_scales: fp8 mode only, [T][d/128] fp32 (see moe_quantize_fp8)
  * topk_ids: [T][k] int32, -1 = masked slot
  * topk_w:   [T][k] fp32 routing weights
- * out:      [T][d] bf16 */
+ * out:      [T][d] bf16
+ * layer_id: one int32 in device memory, the layer whose weights the GEMMs
+ *           use, read on the device when they run (so it may be written by
+ *           earlier work on the stream after the host enqueued this
+ *           micro-batch); NULL means layer 0.  A value outside
+ *           [0, n_layers) is clamped into range and reported by
+ *           moe_stage_sync as MOE_EBADLAYER. */
 typedef struct {
     int32_t        n_tokens;
     const void    *x;
@@ -124,6 +140,7 @@ typedef struct {
     const float   *topk_w;
     void          *out;
     int32_t        combine_mode;   /* MOE_COMBINE_* */
+    const int32_t *layer_id;
 } moe_microbatch;
 
 /* Device pointers into one slot's workspace (for tests and inspection).
@@ -145,9 +162,11 @@ typedef struct {
     int32_t  n_tokens;        /* T of the micro-batch last dispatched here */
 } moe_dispatch_view;
 
-/* Validates `desc`, copies the weights into stage-owned HBM (packed for the
- * grouped GEMM) and allocates all workspace for n_slots micro-batches of up
- * to max_tokens tokens.  Synchronous.  On error *out is NULL. */
+/* Validates `desc`, copies the weights of its n_layers layers
+ * (weights[0 .. n_layers-1]) into stage-owned HBM, packed for the grouped
+ * GEMM, builds the on-device table of the layers' weight addresses, and
+ * allocates all workspace for n_slots micro-batches of up to max_tokens
+ * tokens.  Synchronous.  On error *out is NULL. */
 MOE_API moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *weights,
                             moe_stage **out);
 
@@ -189,8 +208,9 @@ MOE_API moe_status moe_quantize_fp8(const void *x_bf16, int32_t n_tokens, int32_
 MOE_API moe_status moe_stage_query(moe_stage *stage, int32_t slot, moe_dispatch_view *out);
 
 /* Waits until every slot's enqueued work has completed and returns (then
- * clears) the sticky device error: MOE_EBADID if a kernel saw an invalid
- * expert id since the last sync, else MOE_OK (or MOE_EHIP). */
+ * clears) the sticky device errors: MOE_EBADID if a kernel saw an invalid
+ * expert id since the last sync, else MOE_EBADLAYER if one saw an invalid
+ * layer id, else MOE_OK (or MOE_EHIP). */
 MOE_API moe_status moe_stage_sync(moe_stage *stage);
 
 /* Per-kernel timing with HIP events, for measurement (off by default).
@@ -198,8 +218,9 @@ MOE_API moe_status moe_stage_sync(moe_stage *stage);
  * kernel groups on the launch stream (this creates events, i.e. allocates
  * host-side runtime objects).  Kinds, in order: 0 dispatch index
  * (histogram, scan, scatter), 1 row gather (fp8 only; in bf16 it is part of
- * kind 2), 2 grouped GEMM gate/up with the SiLU*up epilogue, 3 grouped GEMM
- * down, 4 combine, 5 fp8 quantisation of h. */
+ * kind 2), 2 grouped GEMM gate/up with the SiLU*up epilogue (fp8: and the
+ * quantisation of h), 3 grouped GEMM down, 4 combine, 5 reserved (no
+ * longer recorded). */
 #define MOE_PROF_KINDS 6
 MOE_API moe_status moe_stage_profile(moe_stage *stage, int32_t enable);
 

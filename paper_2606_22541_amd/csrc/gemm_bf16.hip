@@ -191,6 +191,9 @@ void k_gemm_bf16(GemmArgs a)
     w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = w.wave >> 2, wn = w.wave & 3;        // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
+    const void *Bw;
+    const float *Bsw;
+    resolve_weights(a, Bw, Bsw);
     const int NT = (N + kBN - 1) / kBN;
     const int32_t *tbase = a.large_all ? a.groups.mt_base : a.groups.lt_base;
     const int total = __builtin_amdgcn_readfirstlane(tbase[a.G] * NT);
@@ -226,7 +229,7 @@ void k_gemm_bf16(GemmArgs a)
         const bf16 *A = indexed ? (const bf16 *)a.A_routed
                                 : (const bf16 *)(sh ? a.A_shared : a.A_routed) + (int64_t)row0 * K;
         // the tile's column blocks n0/32 .. n0/32 + 7 are contiguous
-        const bf16 *B = (const bf16 *)a.B + ((int64_t)g * N + n0) * K;
+        const bf16 *B = (const bf16 *)Bw + ((int64_t)g * N + n0) * K;
         Tile t;
         t.ra = make_rsrc(A, (indexed ? a.A_routed_rows : (int64_t)rows_valid) * K * 2);
         {

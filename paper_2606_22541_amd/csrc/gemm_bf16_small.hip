@@ -246,6 +246,9 @@ void k_gemm_bf16_small(GemmArgs a)
     w.kh = w.wave >> 1;
     w.ch = w.wave & 1;
     const int N = a.N, K = a.K;
+    const void *Bw;
+    const float *Bsw;
+    resolve_weights(a, Bw, Bsw);
     const int NT = (N + kTNs - 1) / kTNs;
     const int total = __builtin_amdgcn_readfirstlane(a.groups.st_base[a.G] * NT);
     const int P = gridDim.x;
@@ -278,7 +281,7 @@ void k_gemm_bf16_small(GemmArgs a)
         const bool indexed = a.A_index != nullptr && !sh;
         const bf16 *A = indexed ? (const bf16 *)a.A_routed
                                 : (const bf16 *)(sh ? a.A_shared : a.A_routed) + (int64_t)t.row0 * K;
-        const bf16 *B = (const bf16 *)a.B + ((int64_t)g * N + t.n0) * K;
+        const bf16 *B = (const bf16 *)Bw + ((int64_t)g * N + t.n0) * K;
         t.ra = rsrc_s(A, (indexed ? a.A_routed_rows : (int64_t)t.rows_valid) * K * 2);
 #pragma unroll
         for (int i = 0; i < 6; ++i)

@@ -196,6 +196,9 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
     const int lane = w.lane;
     const int wm = w.wave >> 2, wn = w.wave & 3;        // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
+    const void *Bw;
+    const float *Bsw;
+    resolve_weights(a, Bw, Bsw);
     const int NT = (N + kBN - 1) / kBN;
     const int32_t *tbase = kSmall ? a.groups.st_base : a.large_all ? a.groups.mt_base : a.groups.lt_base;
     const int total = __builtin_amdgcn_readfirstlane(tbase[a.G] * NT);
@@ -244,7 +247,7 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
         const bool sh = (g == a.shared_group);
         const uint8_t *A = (const uint8_t *)(sh ? a.A_shared : a.A_routed) + (int64_t)row0 * K;
         const float *As = (sh ? a.As_shared : a.As_routed) + row0;      // [K/128][ld]
-        const uint8_t *B = (const uint8_t *)a.B + ((int64_t)g * N + n0) * K;
+        const uint8_t *B = (const uint8_t *)Bw + ((int64_t)g * N + n0) * K;
         Tile8 t;
         t.KT = K / kGrpB;
         t.s_ld = sh ? lds_rows_shared : lds_rows_routed;
@@ -261,11 +264,11 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
         if constexpr (SWIGLU) {
             // [G][f/128][gate, up][K/128]: tile nt covers gate/up scale block nt
             const int f = N / 2;
-            t.sbp = a.Bs + (((int64_t)g * (f / 128) + nt) * 2 + (wn & 1)) * t.KT;
+            t.sbp = Bsw + (((int64_t)g * (f / 128) + nt) * 2 + (wn & 1)) * t.KT;
         } else {
             // [G][N/128][K/128]: wave columns n0 + 64 wn .. + 63
             const int nb = min(2 * nt + (wn >> 1), N / 128 - 1);
-            t.sbp = a.Bs + ((int64_t)g * (N / 128) + nb) * t.KT;
+            t.sbp = Bsw + ((int64_t)g * (N / 128) + nb) * t.KT;
         }
 
         f32x4 acc[RB][4];

@@ -38,6 +38,13 @@ hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_
 hipError_t launch_transpose_scales(const float *src, int32_t rows, int32_t cols, float *dst,
                                    int32_t ld, hipStream_t s);
 
+// Packed weights of one layer (device addresses); the stage keeps a device
+// array of these, one per layer.
+struct LayerWeights {
+    const void *w1, *w2;      // gate/up and down, in MFMA fragment order
+    const float *s1, *s2;     // fp8 block scales (null in bf16)
+};
+
 struct GemmArgs {
     const void *A_routed;    // [rows][K] (rows of X_perm or H), or x itself when A_index is set
     const void *A_shared;    // [T][K] (x or H_shared) for group E_loc, if shared
@@ -60,7 +67,33 @@ struct GemmArgs {
     const int32_t *A_index;
     int32_t A_index_div;
     int64_t A_routed_rows;
+    // Layer-oblivious weights: with layer_id set, B and Bs are taken on the
+    // device from layers[*layer_id] (w1/s1, or w2/s2 when `down`); an id
+    // outside [0, n_layers) is clamped and flagged in err.
+    const int32_t *layer_id;
+    const LayerWeights *layers;
+    int32_t n_layers;
+    int32_t down;
+    int32_t *err;
 };
+
+// The weights a GEMM launch uses: a.B / a.Bs, or the ones of the layer named
+// in device memory (read once per workgroup; every wave gets the same value).
+__device__ __forceinline__ void resolve_weights(const GemmArgs &a, const void *&B, const float *&Bs)
+{
+    B = a.B;
+    Bs = a.Bs;
+    if (a.layer_id) {
+        int l = __builtin_amdgcn_readfirstlane(*a.layer_id);
+        if (l < 0 || l >= a.n_layers) {
+            if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(a.err, kErrBadLayer);
+            l = l < 0 ? 0 : a.n_layers - 1;
+        }
+        const LayerWeights &lw = a.layers[l];
+        B = a.down ? lw.w2 : lw.w1;
+        Bs = a.down ? lw.s2 : lw.s1;
+    }
+}
 
 // bf16 grouped GEMM.  swiglu = true: B is the packed [gate|up] matrix
 // (N = 2f) and C receives SiLU(gate) * up as [rows][f] bf16; otherwise C

@@ -41,7 +41,8 @@ struct SlotWs {
 
 struct Sizes {
     int64_t G, cap, nb_max, eb, n_slots_tok;
-    int64_t w1, w2, s1, s2;                 // bytes
+    int64_t w1, w2, s1, s2;                 // bytes, all layers
+    int64_t w1l, w2l, s1l, s2l;             // bytes of one layer
     int64_t per_slot;                       // bytes
 };
 
@@ -58,6 +59,7 @@ bool desc_ok(const moe_stage_desc *d)
     if (d->max_tokens < 0 || d->n_slots < 1 || d->n_slots > 64) return false;
     if (d->dtype != MOE_DTYPE_BF16 && d->dtype != MOE_DTYPE_FP8_E4M3_B128) return false;
     if (d->has_shared_expert != 0 && d->has_shared_expert != 1) return false;
+    if (d->n_layers < 1 || d->n_layers > kMaxLayers) return false;
     // 32-bit slot and row indices; 32-bit byte offsets inside one GEMM tile
     if ((int64_t)d->max_tokens * d->top_k >= (int64_t)1 << 31) return false;
     if ((int64_t)256 * d->d_model * 2 >= (int64_t)1 << 31) return false;
@@ -79,10 +81,14 @@ Sizes sizes_of(const moe_stage_desc *d)
     s.n_slots_tok = T * k;
     s.nb_max = (s.n_slots_tok + kDispatchChunk - 1) / kDispatchChunk;
     if (s.nb_max < 1) s.nb_max = 1;
-    s.w1 = align256(s.G * 2 * F * D * s.eb);
-    s.w2 = align256(s.G * D * F * s.eb);
-    s.s1 = fp8 ? align256(s.G * (2 * F / 128) * (D / 128) * 4) : 0;
-    s.s2 = fp8 ? align256(s.G * (D / 128) * (F / 128) * 4) : 0;
+    s.w1l = align256(s.G * 2 * F * D * s.eb);
+    s.w2l = align256(s.G * D * F * s.eb);
+    s.s1l = fp8 ? align256(s.G * (2 * F / 128) * (D / 128) * 4) : 0;
+    s.s2l = fp8 ? align256(s.G * (D / 128) * (F / 128) * 4) : 0;
+    s.w1 = s.w1l * d->n_layers;
+    s.w2 = s.w2l * d->n_layers;
+    s.s1 = s.s1l * d->n_layers;
+    s.s2 = s.s2l * d->n_layers;
     const int64_t cap1 = s.cap > 0 ? s.cap : 1;
     const int64_t T1 = T > 0 ? T : 1;
     int64_t b = 0;
@@ -117,6 +123,7 @@ struct moe_stage {
     int num_cus = 0;
     void *w1 = nullptr, *w2 = nullptr;
     float *s1 = nullptr, *s2 = nullptr;
+    LayerWeights *layers = nullptr;   // device table, one entry per layer
     int32_t *err = nullptr;
     hipStream_t own = nullptr;
     std::vector<SlotWs> slots;
@@ -193,6 +200,61 @@ moe_status record(SlotWs &sl, hipStream_t s)
     return MOE_OK;
 }
 
+// Packs one layer's weights into w1/w2 (and fp8 scales into s1/s2) in MFMA
+// fragment order; the shared expert is group E_loc.  [gate|up] is
+// interleaved by 16 rows (bf16) or 64 rows (fp8).
+hipError_t pack_layer(const moe_stage_desc *d, const Sizes &z, const moe_weights *w, void *w1,
+                      void *w2, float *s1, float *s2, hipStream_t s)
+{
+    const bool fp8 = d->dtype == MOE_DTYPE_FP8_E4M3_B128;
+    const int64_t D = d->d_model, F = d->d_ff, El = d->n_local_experts;
+    hipError_t e = hipSuccess;
+    const int64_t w1_mat = 2 * F * D * z.eb, w2_mat = D * F * z.eb;
+    if (fp8) {
+        e = launch_pack_frag_fp8(w->w_gate, w->w_up, w1, (int32_t)El, (int32_t)(2 * F),
+                                 (int32_t)D, kInterleaveFp8, s);
+        if (e == hipSuccess)
+            e = launch_pack_frag_fp8(w->w_down, nullptr, w2, (int32_t)El, (int32_t)D,
+                                     (int32_t)F, 0, s);
+        if (e == hipSuccess && d->has_shared_expert) {
+            e = launch_pack_frag_fp8(w->sh_gate, w->sh_up, (char *)w1 + El * w1_mat, 1,
+                                     (int32_t)(2 * F), (int32_t)D, kInterleaveFp8, s);
+            if (e == hipSuccess)
+                e = launch_pack_frag_fp8(w->sh_down, nullptr, (char *)w2 + El * w2_mat, 1,
+                                         (int32_t)D, (int32_t)F, 0, s);
+        }
+    } else {
+        e = launch_pack_frag_bf16(w->w_gate, w->w_up, w1, (int32_t)El, (int32_t)(2 * F),
+                                  (int32_t)D, kInterleaveBf16, s);
+        if (e == hipSuccess)
+            e = launch_pack_frag_bf16(w->w_down, nullptr, w2, (int32_t)El, (int32_t)D,
+                                      (int32_t)F, 0, s);
+        if (e == hipSuccess && d->has_shared_expert) {
+            e = launch_pack_frag_bf16(w->sh_gate, w->sh_up, (char *)w1 + El * w1_mat, 1,
+                                      (int32_t)(2 * F), (int32_t)D, kInterleaveBf16, s);
+            if (e == hipSuccess)
+                e = launch_pack_frag_bf16(w->sh_down, nullptr, (char *)w2 + El * w2_mat, 1,
+                                          (int32_t)D, (int32_t)F, 0, s);
+        }
+    }
+    if (e == hipSuccess && fp8) {
+        const int64_t s1_mat = (2 * F / 128) * (D / 128), s2_mat = (D / 128) * (F / 128);
+        e = launch_pack_gate_up_scales(w->s_gate, w->s_up, s1, (int32_t)El, (int32_t)F,
+                                       (int32_t)D, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(s2, w->s_down, (size_t)(El * s2_mat * 4),
+                               hipMemcpyDeviceToDevice, s);
+        if (e == hipSuccess && d->has_shared_expert) {
+            e = launch_pack_gate_up_scales(w->sh_s_gate, w->sh_s_up, s1 + El * s1_mat, 1,
+                                           (int32_t)F, (int32_t)D, s);
+            if (e == hipSuccess)
+                e = hipMemcpyAsync(s2 + El * s2_mat, w->sh_s_down, (size_t)(s2_mat * 4),
+                                   hipMemcpyDeviceToDevice, s);
+        }
+    }
+    return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -207,6 +269,7 @@ const char *moe_status_string(moe_status s)
     case MOE_EBADID: return "expert id outside [-1, n_experts) seen on the device";
     case MOE_EUNSUPPORTED: return "unsupported shape or mode";
     case MOE_EBUSY: return "slot busy";
+    case MOE_EBADLAYER: return "layer id outside [0, n_layers) seen on the device (clamped)";
     default: return "unknown status";
     }
 }
@@ -216,7 +279,8 @@ moe_status moe_stage_workspace_bytes(const moe_stage_desc *desc, int64_t *bytes)
     if (!bytes) return MOE_EINVAL;
     if (!desc_ok(desc)) return MOE_EINVAL;
     Sizes s = sizes_of(desc);
-    *bytes = s.w1 + s.w2 + s.s1 + s.s2 + 256 + s.per_slot * desc->n_slots;
+    *bytes = s.w1 + s.w2 + s.s1 + s.s2 + 256 + align256(desc->n_layers * (int64_t)sizeof(LayerWeights)) +
+             s.per_slot * desc->n_slots;
     return MOE_OK;
 }
 
@@ -226,11 +290,14 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
     *out = nullptr;
     if (!desc_ok(desc) || !w) return MOE_EINVAL;
     const bool fp8 = desc->dtype == MOE_DTYPE_FP8_E4M3_B128;
-    if (!w->w_gate || !w->w_up || !w->w_down) return MOE_EINVAL;
-    if (fp8 && (!w->s_gate || !w->s_up || !w->s_down)) return MOE_EINVAL;
-    if (desc->has_shared_expert) {
-        if (!w->sh_gate || !w->sh_up || !w->sh_down) return MOE_EINVAL;
-        if (fp8 && (!w->sh_s_gate || !w->sh_s_up || !w->sh_s_down)) return MOE_EINVAL;
+    for (int l = 0; l < desc->n_layers; ++l) {
+        const moe_weights &wl = w[l];
+        if (!wl.w_gate || !wl.w_up || !wl.w_down) return MOE_EINVAL;
+        if (fp8 && (!wl.s_gate || !wl.s_up || !wl.s_down)) return MOE_EINVAL;
+        if (desc->has_shared_expert) {
+            if (!wl.sh_gate || !wl.sh_up || !wl.sh_down) return MOE_EINVAL;
+            if (fp8 && (!wl.sh_s_gate || !wl.sh_s_up || !wl.sh_s_down)) return MOE_EINVAL;
+        }
     }
 
     moe_stage *st = new (std::nothrow) moe_stage();
@@ -246,58 +313,28 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
         return MOE_EHIP;
     }
     const int64_t D = desc->d_model, F = desc->d_ff, El = desc->n_local_experts;
-    bool ok = alloc(st, &st->w1, z.w1) && alloc(st, &st->w2, z.w2) && alloc(st, &st->err, 4);
+    bool ok = alloc(st, &st->w1, z.w1) && alloc(st, &st->w2, z.w2) && alloc(st, &st->err, 4) &&
+              alloc(st, &st->layers, desc->n_layers * (int64_t)sizeof(LayerWeights));
     if (ok && fp8) ok = alloc(st, &st->s1, z.s1) && alloc(st, &st->s2, z.s2);
     if (!ok) {
         release(st);
         return MOE_ENOMEM;
     }
-    // Pack the weights in MFMA fragment order; the shared expert is group
-    // E_loc.  [gate|up] is interleaved by 16 rows (bf16) or 64 rows (fp8).
+    // Pack every layer's weights and build the device table of their addresses.
     hipError_t e = hipSuccess;
-    const int64_t w1_mat = 2 * F * D * z.eb, w2_mat = D * F * z.eb;
-    if (fp8) {
-        e = launch_pack_frag_fp8(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)(2 * F),
-                                 (int32_t)D, kInterleaveFp8, st->own);
-        if (e == hipSuccess)
-            e = launch_pack_frag_fp8(w->w_down, nullptr, st->w2, (int32_t)El, (int32_t)D,
-                                     (int32_t)F, 0, st->own);
-        if (e == hipSuccess && desc->has_shared_expert) {
-            e = launch_pack_frag_fp8(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
-                                     (int32_t)(2 * F), (int32_t)D, kInterleaveFp8, st->own);
-            if (e == hipSuccess)
-                e = launch_pack_frag_fp8(w->sh_down, nullptr, (char *)st->w2 + El * w2_mat, 1,
-                                         (int32_t)D, (int32_t)F, 0, st->own);
-        }
-    } else {
-        e = launch_pack_frag_bf16(w->w_gate, w->w_up, st->w1, (int32_t)El, (int32_t)(2 * F),
-                                  (int32_t)D, kInterleaveBf16, st->own);
-        if (e == hipSuccess)
-            e = launch_pack_frag_bf16(w->w_down, nullptr, st->w2, (int32_t)El, (int32_t)D,
-                                      (int32_t)F, 0, st->own);
-        if (e == hipSuccess && desc->has_shared_expert) {
-            e = launch_pack_frag_bf16(w->sh_gate, w->sh_up, (char *)st->w1 + El * w1_mat, 1,
-                                      (int32_t)(2 * F), (int32_t)D, kInterleaveBf16, st->own);
-            if (e == hipSuccess)
-                e = launch_pack_frag_bf16(w->sh_down, nullptr, (char *)st->w2 + El * w2_mat, 1,
-                                          (int32_t)D, (int32_t)F, 0, st->own);
-        }
+    std::vector<LayerWeights> table(desc->n_layers);
+    for (int l = 0; l < desc->n_layers && e == hipSuccess; ++l) {
+        LayerWeights &lw = table[l];
+        lw.w1 = (char *)st->w1 + l * z.w1l;
+        lw.w2 = (char *)st->w2 + l * z.w2l;
+        lw.s1 = fp8 ? (float *)((char *)st->s1 + l * z.s1l) : nullptr;
+        lw.s2 = fp8 ? (float *)((char *)st->s2 + l * z.s2l) : nullptr;
+        e = pack_layer(desc, z, &w[l], (void *)lw.w1, (void *)lw.w2, (float *)lw.s1,
+                       (float *)lw.s2, st->own);
     }
-    if (e == hipSuccess && fp8) {
-        const int64_t s1_mat = (2 * F / 128) * (D / 128), s2_mat = (D / 128) * (F / 128);
-        e = launch_pack_gate_up_scales(w->s_gate, w->s_up, st->s1, (int32_t)El, (int32_t)F,
-                                       (int32_t)D, st->own);
-        if (e == hipSuccess)
-            e = hipMemcpyAsync(st->s2, w->s_down, (size_t)(El * s2_mat * 4),
-                               hipMemcpyDeviceToDevice, st->own);
-        if (e == hipSuccess && desc->has_shared_expert) {
-            e = launch_pack_gate_up_scales(w->sh_s_gate, w->sh_s_up, st->s1 + El * s1_mat, 1,
-                                           (int32_t)F, (int32_t)D, st->own);
-            if (e == hipSuccess)
-                e = hipMemcpyAsync(st->s2 + El * s2_mat, w->sh_s_down, (size_t)(s2_mat * 4),
-                                   hipMemcpyDeviceToDevice, st->own);
-        }
-    }
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(st->layers, table.data(), table.size() * sizeof(LayerWeights),
+                           hipMemcpyHostToDevice, st->own);
     if (e == hipSuccess) e = hipMemsetAsync(st->err, 0, 4, st->own);
     if (e != hipSuccess) {
         release(st);
@@ -447,6 +484,11 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     g1.shared_group = d.has_shared_expert ? d.n_local_experts : -1;
     g1.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base};
     g1.G = (int32_t)st->sz.G;
+    g1.layer_id = sl.mb.layer_id;   // weights named on the device (NULL: layer 0)
+    g1.layers = st->layers;
+    g1.n_layers = d.n_layers;
+    g1.down = 0;
+    g1.err = st->err;
 
     GemmArgs g2 = g1;
     g2.A_index = nullptr;            // H rows are already grouped by expert
@@ -460,6 +502,7 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     g2.As_shared = sl.h_sh_s;
     g2.B = st->w2;
     g2.Bs = st->s2;
+    g2.down = 1;
     g2.C_routed = sl.y_perm;
     g2.C_shared = sl.y_sh;
     g2.N = d.d_model;
@@ -633,7 +676,7 @@ moe_status moe_stage_sync(moe_stage *st)
         if (hipMemsetAsync(st->err, 0, 4, st->own) != hipSuccess ||
             hipStreamSynchronize(st->own) != hipSuccess)
             return MOE_EHIP;
-        return MOE_EBADID;
+        return (err & kErrBadId) ? MOE_EBADID : MOE_EBADLAYER;
     }
     return MOE_OK;
 }

@@ -25,6 +25,7 @@ MOE_EHIP = -3
 MOE_EBADID = -4
 MOE_EUNSUPPORTED = -5
 MOE_EBUSY = -6
+MOE_EBADLAYER = -7
 MOE_DTYPE_BF16 = 0
 MOE_DTYPE_FP8_E4M3_B128 = 1
 MOE_COMBINE_OVERWRITE = 0
@@ -45,7 +46,7 @@ PROF_KIND_NAMES = ("dispatch_index", "gather", "gemm_gate_up_swiglu", "gemm_down
 class moe_stage_desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "d_model", "d_ff", "n_experts", "first_local_expert", "n_local_experts", "top_k",
-        "max_tokens", "n_slots", "dtype", "has_shared_expert")]
+        "max_tokens", "n_slots", "dtype", "has_shared_expert", "n_layers")]
 
 
 class moe_weights(ctypes.Structure):
@@ -57,7 +58,7 @@ class moe_weights(ctypes.Structure):
 class moe_microbatch(ctypes.Structure):
     _fields_ = [("n_tokens", ctypes.c_int32), ("x", ctypes.c_void_p), ("x_scales", ctypes.c_void_p),
                 ("topk_ids", ctypes.c_void_p), ("topk_w", ctypes.c_void_p), ("out", ctypes.c_void_p),
-                ("combine_mode", ctypes.c_int32)]
+                ("combine_mode", ctypes.c_int32), ("layer_id", ctypes.c_void_p)]
 
 
 class moe_dispatch_view(ctypes.Structure):
@@ -144,9 +145,9 @@ def _stream(s) -> Optional[int]:
 
 
 def make_desc(d_model, d_ff, n_experts, first_local_expert, n_local_experts, top_k, max_tokens,
-              n_slots=1, dtype=MOE_DTYPE_BF16, has_shared_expert=0) -> moe_stage_desc:
+              n_slots=1, dtype=MOE_DTYPE_BF16, has_shared_expert=0, n_layers=1) -> moe_stage_desc:
     return moe_stage_desc(d_model, d_ff, n_experts, first_local_expert, n_local_experts, top_k,
-                          max_tokens, n_slots, dtype, int(has_shared_expert))
+                          max_tokens, n_slots, dtype, int(has_shared_expert), int(n_layers))
 
 
 def make_weights(w_gate, w_up, w_down, s_gate=None, s_up=None, s_down=None, sh_gate=None,
@@ -157,15 +158,20 @@ def make_weights(w_gate, w_up, w_down, s_gate=None, s_up=None, s_down=None, sh_g
 
 
 def make_microbatch(n_tokens, x, topk_ids, topk_w, out, x_scales=None,
-                    combine_mode=MOE_COMBINE_OVERWRITE) -> moe_microbatch:
+                    combine_mode=MOE_COMBINE_OVERWRITE, layer_id=None) -> moe_microbatch:
+    """layer_id: device int32 (tensor or address) naming the layer, or None."""
     return moe_microbatch(int(n_tokens), _ptr(x), _ptr(x_scales), _ptr(topk_ids), _ptr(topk_w),
-                          _ptr(out), int(combine_mode))
+                          _ptr(out), int(combine_mode), _ptr(layer_id))
 
 
-def moe_stage_create(desc: moe_stage_desc, weights: moe_weights) -> int:
+def moe_stage_create(desc: moe_stage_desc, weights) -> int:
+    """weights: one moe_weights, or a sequence of desc.n_layers of them."""
+    if isinstance(weights, moe_weights):
+        weights = [weights]
+    arr = (moe_weights * len(weights))(*weights)
     h = ctypes.c_void_p()
-    _check(load_library().moe_stage_create(ctypes.byref(desc), ctypes.byref(weights),
-                                           ctypes.byref(h)), "moe_stage_create")
+    _check(load_library().moe_stage_create(ctypes.byref(desc), arr, ctypes.byref(h)),
+           "moe_stage_create")
     return h.value
 
 

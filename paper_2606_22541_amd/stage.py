@@ -38,24 +38,28 @@ def device_to_numpy(ptr: int, count: int, dtype) -> np.ndarray:
 
 
 class ExpertStage:
-    """One device's share of experts, created from generator weights."""
+    """One device's share of experts, created from generator weights (one
+    ExpertWeights, or a list of them: one per layer)."""
 
     def __init__(self, cfg, weights, n_slots: int = 1, max_tokens: Optional[int] = None):
         self.cfg = cfg
         self.fp8 = cfg.dtype == "fp8"
         self.max_tokens = cfg.max_tokens if max_tokens is None else max_tokens
+        layers = list(weights) if isinstance(weights, (list, tuple)) else [weights]
+        self.n_layers = len(layers)
         self.desc = C.make_desc(cfg.d, cfg.f, cfg.E, cfg.e0, cfg.E_loc, cfg.k, self.max_tokens,
                                 n_slots, C.MOE_DTYPE_FP8_E4M3_B128 if self.fp8 else C.MOE_DTYPE_BF16,
-                                int(cfg.has_shared))
-        w = weights
-        wts = C.make_weights(w.w_gate, w.w_up, w.w_down, w.s_gate, w.s_up, w.s_down,
-                             w.sh_gate, w.sh_up, w.sh_down, w.sh_s_gate, w.sh_s_up, w.sh_s_down)
+                                int(cfg.has_shared), self.n_layers)
+        wts = [C.make_weights(w.w_gate, w.w_up, w.w_down, w.s_gate, w.s_up, w.s_down,
+                              w.sh_gate, w.sh_up, w.sh_down, w.sh_s_gate, w.sh_s_up, w.sh_s_down)
+               for w in layers]
         torch.cuda.synchronize()
         self.handle = C.moe_stage_create(self.desc, wts)
         self._keep = {}
 
-    def microbatch(self, x, ids, w, out, x_scales=None, mode=C.MOE_COMBINE_OVERWRITE):
-        return C.make_microbatch(ids.shape[0], x, ids, w, out, x_scales, mode)
+    def microbatch(self, x, ids, w, out, x_scales=None, mode=C.MOE_COMBINE_OVERWRITE,
+                   layer_id=None):
+        return C.make_microbatch(ids.shape[0], x, ids, w, out, x_scales, mode, layer_id)
 
     def submit(self, mb, stream=None) -> int:
         return C.moe_stage_submit_microbatch(self.handle, mb, stream)

@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 def test_status_strings(lib):
     for code in (C.MOE_OK, C.MOE_EINVAL, C.MOE_ENOMEM, C.MOE_EHIP, C.MOE_EBADID,
-                 C.MOE_EUNSUPPORTED, C.MOE_EBUSY):
+                 C.MOE_EUNSUPPORTED, C.MOE_EBUSY, C.MOE_EBADLAYER):
         assert C.moe_status_string(code) not in ("", "unknown status")
     assert C.moe_status_string(12345) == "unknown status"
 
@@ -77,14 +77,28 @@ def test_workspace_bytes_host_only(lib):
     assert rows * fp8_row <= f_slot < rows * fp8_row + 8 * 2**20
 
 
+def test_workspace_bytes_scale_with_layers(lib):
+    """n_layers copies of the packed weights (and, in fp8, of their scales);
+    the workspace slots do not depend on the layer count."""
+    for dtype, eb in ((C.MOE_DTYPE_BF16, 2), (C.MOE_DTYPE_FP8_E4M3_B128, 1)):
+        one = C.moe_stage_workspace_bytes(
+            C.make_desc(7168, 2048, 256, 0, 8, 8, 4096, n_slots=2, dtype=dtype, n_layers=1))
+        five = C.moe_stage_workspace_bytes(
+            C.make_desc(7168, 2048, 256, 0, 8, 8, 4096, n_slots=2, dtype=dtype, n_layers=5))
+        per_layer = (five - one) / 4
+        w = 8 * 3 * 2048 * 7168 * eb
+        assert w <= per_layer < w + 2**20
+
+
 @pytest.mark.parametrize("bad", [
     dict(d_model=200), dict(d_ff=100), dict(n_experts=0), dict(n_experts=2000),
     dict(n_local_experts=0), dict(first_local_expert=250), dict(top_k=0), dict(top_k=33),
     dict(max_tokens=-1), dict(n_slots=0), dict(dtype=7), dict(has_shared_expert=2),
+    dict(n_layers=0), dict(n_layers=-3), dict(n_layers=1025),
 ])
 def test_invalid_desc_rejected(lib, bad):
     args = dict(d_model=256, d_ff=128, n_experts=8, first_local_expert=0, n_local_experts=4,
-                top_k=2, max_tokens=64, n_slots=1, dtype=0, has_shared_expert=0)
+                top_k=2, max_tokens=64, n_slots=1, dtype=0, has_shared_expert=0, n_layers=1)
     args.update(bad)
     d = C.moe_stage_desc(**args)
     with pytest.raises(C.MoEStageError) as e:
