@@ -256,6 +256,63 @@ def describe(r):
         per=r["n_local_slots"] // c.E_loc)
 
 
+SWEEP_TOKENS = (512, 1024, 2048, 4096, 8192, 12288, 16384, 24576, 32768)
+
+
+def run_sweep(tokens=SWEEP_TOKENS, steps=10, warmup=5):
+    """MoE-stage latency against micro-batch size for the c1 expert share
+    (7168 x 2048, 8 of 256 experts local, top-8, uniform routing, bf16): the
+    single-GPU analog of the paper's latency-vs-tokens curve under perfect
+    balance, which is flat while the weights' HBM stream dominates and turns
+    linear once the grouped GEMM is MFMA-bound.  The knee is where a flat
+    line through the smallest batch meets the line through the two largest."""
+    import torch
+    from paper_2606_22541_amd import inputs
+    from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
+
+    cfg = inputs.CONFIGS["c1"]
+    w = inputs.make_weights(cfg, "cuda")
+    stage = ExpertStage(cfg, w, n_slots=2, max_tokens=max(tokens))
+    del w
+    main = torch.cuda.Stream()
+    pts = []
+    for T in tokens:
+        c = inputs.scaled(cfg, name="c1_T%d" % T, lengths=(T,))
+        mb = inputs.make_microbatches(c, "cuda")[0]
+        ids, wt = to_device_routing(mb.ids, mb.w)
+        outs = [torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+        mbs = [stage.microbatch(mb.x, ids, wt, o) for o in outs]
+        torch.cuda.synchronize()
+        for i in range(warmup):
+            stage.submit(mbs[i % 2], main)
+        stage.sync()
+        torch.cuda.synchronize()
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record(main)
+        for i in range(steps):
+            stage.submit(mbs[i % 2], main)
+        end.record(main)
+        stage.sync()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end) / steps
+        local = int(np.count_nonzero((mb.ids >= cfg.e0) & (mb.ids < cfg.e0 + cfg.E_loc)))
+        pts.append({"T": T, "ms": round(ms, 4), "us_per_token": round(ms * 1e3 / T, 4),
+                    "rows_per_expert": round(local / cfg.E_loc, 1)})
+        del mbs, outs
+    stage.close()
+    t0, m0 = pts[0]["T"], pts[0]["ms"]
+    (ta, ma), (tb, mb_) = [(p["T"], p["ms"]) for p in pts[-2:]]
+    slope = (mb_ - ma) / (tb - ta)
+    knee = tb - (mb_ - m0) / slope if slope > 0 else None
+    return {"workload": "c1 expert share at T tokens (d=7168, f=2048, 8 of 256 experts local, "
+                        "top-8, uniform, bf16)",
+            "points": pts,
+            "knee_tokens": round(knee) if knee else None,
+            "knee_rows_per_expert": round(knee * cfg.k / cfg.E) if knee else None,
+            "ms_per_1k_tokens_linear": round(slope * 1e3, 4)}
+
+
 def run_layers(n_layers, passes=3):
     """Layer-oblivious submission against host-in-the-loop dispatch, on one
     stage holding n_layers copies of the c1 expert share (7168 x 2048, 8
@@ -365,6 +422,8 @@ def main():
     ap.add_argument("--secondary", default="c1p,c3,c2,c4",
                     help="comma-separated further workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the latency-vs-tokens sweep of the c1 expert share")
     ap.add_argument("--layers", type=int, default=8,
                     help="layers for the layer-oblivious dispatch measurement (0: skip)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -424,6 +483,9 @@ def main():
             "kernels": stream_rooflines(sec),
         }
         _log("[bench] %s done" % name)
+    if not args.no_sweep:
+        line["token_sweep"] = run_sweep()
+        _log("[bench] token sweep done")
     if args.layers > 0:
         line["layer_oblivious"] = run_layers(args.layers)
         _log("[bench] layer-oblivious dispatch done")
