@@ -256,6 +256,134 @@ def describe(r):
         per=r["n_local_slots"] // c.E_loc)
 
 
+def run_pipelined(name="c1", n_streams=3, steps=40, warmup=30, repeats=3):
+    """Throughput of a stream of micro-batches of workload `name` with up to
+    n_streams of them in flight: micro-batch i is submitted on stream
+    i % n_streams (per-micro-batch streams, section 3.4.1), consecutive ones
+    are not joined, and the slot ring's device-side waits are the only
+    dependency between them.  Returns the best of `repeats` timed regions."""
+    import torch
+    from paper_2606_22541_amd import inputs
+    from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
+
+    cfg = inputs.CONFIGS[name]
+    w = inputs.make_weights(cfg, "cuda")
+    mb = inputs.make_microbatches(cfg, "cuda")[0]
+    T = mb.ids.shape[0]
+    ids, wt = to_device_routing(mb.ids, mb.w)
+    nb = n_streams + 1                       # distinct input/output buffer sets
+    xs = [mb.x.clone() for _ in range(nb)]
+    outs = [torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda") for _ in range(nb)]
+    stage = ExpertStage(cfg, w, n_slots=nb, max_tokens=T)
+    del w
+    mbs = [stage.microbatch(xs[i], ids, wt, outs[i]) for i in range(nb)]
+    main = torch.cuda.Stream()
+    streams = [torch.cuda.Stream() for _ in range(n_streams)]
+    torch.cuda.synchronize()
+
+    def run(n):
+        go = torch.cuda.Event()
+        go.record(main)
+        for st_ in streams:
+            st_.wait_event(go)
+        for i in range(n):
+            stage.submit(mbs[i % nb], streams[i % n_streams])
+        for st_ in streams:
+            e = torch.cuda.Event()
+            e.record(st_)
+            main.wait_event(e)
+
+    run(warmup)
+    stage.sync()
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(repeats):
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record(main)
+        run(steps)
+        end.record(main)
+        stage.sync()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end) / steps
+        best = ms if best is None else min(best, ms)
+    stage.close()
+    return {"workload": "%s micro-batches (T=%d) submitted round-robin on %d streams, up to %d in "
+                        "flight" % (name, T, n_streams, n_streams),
+            "streams": n_streams, "ms_per_microbatch": round(best, 4),
+            "tokens_per_s": round(T / (best / 1e3), 1)}
+
+
+def run_triple_stream(name="c1", in_flight=3, steps=40, warmup=30, repeats=3):
+    """The paper's three-stream layout on one GPU: dispatch on one stream,
+    the grouped GEMMs on a compute stream, the combine on a third, each
+    micro-batch's steps chained by events and slot reuse guarded by the
+    slot's last combine, so one micro-batch's dispatch and combine run
+    beside another's GEMMs.  Returns the best of `repeats` timed regions."""
+    import torch
+    from paper_2606_22541_amd import inputs
+    from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
+
+    cfg = inputs.CONFIGS[name]
+    w = inputs.make_weights(cfg, "cuda")
+    mb = inputs.make_microbatches(cfg, "cuda")[0]
+    T = mb.ids.shape[0]
+    ids, wt = to_device_routing(mb.ids, mb.w)
+    nb = in_flight + 1
+    xs = [mb.x.clone() for _ in range(nb)]
+    outs = [torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda") for _ in range(nb)]
+    stage = ExpertStage(cfg, w, n_slots=nb, max_tokens=T)
+    del w
+    mbs = [stage.microbatch(xs[i], ids, wt, outs[i]) for i in range(nb)]
+    main = torch.cuda.Stream()
+    D, G, R = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    slot_done = [None] * nb
+
+    def run(n):
+        go = torch.cuda.Event()
+        go.record(main)
+        for st_ in (D, G, R):
+            st_.wait_event(go)
+        for i in range(n):
+            k = i % nb
+            if slot_done[k] is not None:
+                D.wait_event(slot_done[k])
+            stage.dispatch(k, mbs[k], D)
+            e1 = torch.cuda.Event()
+            e1.record(D)
+            G.wait_event(e1)
+            stage.expert_ffn(k, G)
+            e2 = torch.cuda.Event()
+            e2.record(G)
+            R.wait_event(e2)
+            stage.combine(k, R)
+            e3 = torch.cuda.Event()
+            e3.record(R)
+            slot_done[k] = e3
+        e = torch.cuda.Event()
+        e.record(R)
+        main.wait_event(e)
+
+    run(warmup)
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(repeats):
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record(main)
+        run(steps)
+        end.record(main)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end) / steps
+        best = ms if best is None else min(best, ms)
+    stage.sync()
+    torch.cuda.synchronize()
+    stage.close()
+    return {"workload": "%s micro-batches (T=%d), dispatch / grouped GEMMs / combine on three "
+                        "streams, up to %d micro-batches in flight" % (name, T, nb),
+            "ms_per_microbatch": round(best, 4), "tokens_per_s": round(T / (best / 1e3), 1)}
+
+
 SWEEP_TOKENS = (512, 1024, 2048, 4096, 8192, 12288, 16384, 24576, 32768)
 
 
@@ -422,6 +550,11 @@ def main():
     ap.add_argument("--secondary", default="c1p,c3,c2,c4",
                     help="comma-separated further workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pipelined-streams", type=int, default=3,
+                    help="also time the primary workload with this many micro-batches in flight "
+                         "on separate streams (<= 1: skip)")
+    ap.add_argument("--triple-stream", type=int, default=1,
+                    help="also time the dispatch / GEMM / combine three-stream layout (0: skip)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the latency-vs-tokens sweep of the c1 expert share")
     ap.add_argument("--layers", type=int, default=8,
@@ -483,6 +616,12 @@ def main():
             "kernels": stream_rooflines(sec),
         }
         _log("[bench] %s done" % name)
+    if args.pipelined_streams > 1:
+        line["%s_pipelined" % args.workload] = run_pipelined(args.workload, args.pipelined_streams)
+        _log("[bench] pipelined %s done" % args.workload)
+    if args.triple_stream:
+        line["%s_triple_stream" % args.workload] = run_triple_stream(args.workload)
+        _log("[bench] triple-stream %s done" % args.workload)
     if not args.no_sweep:
         line["token_sweep"] = run_sweep()
         _log("[bench] token sweep done")

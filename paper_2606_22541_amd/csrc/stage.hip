@@ -396,6 +396,23 @@ static bool mb_ok(const moe_stage *st, const moe_microbatch *mb)
     return true;
 }
 
+// CUs the kernels of `stream` may run on: the stream's CU mask when it has
+// one (hipExtStreamCreateWithCUMask), else every CU.  The persistent GEMMs
+// size their grids by it, so a masked stream gets one workgroup per CU it
+// may use instead of a second round of workgroups.
+static int stream_cus(const moe_stage *st, hipStream_t s)
+{
+    if (!s) return st->num_cus;
+    uint32_t mask[32] = {};
+    if (hipExtStreamGetCUMask(s, 32, mask) != hipSuccess) {
+        (void)hipGetLastError();
+        return st->num_cus;
+    }
+    int n = 0;
+    for (uint32_t m : mask) n += __builtin_popcount(m);
+    return (n > 0 && n < st->num_cus) ? n : st->num_cus;
+}
+
 // The three phases.  `rec` records the slot's event at the end; a submit
 // records it once, after the combine, since every record is a release that
 // stalls the stream for several microseconds.
@@ -439,7 +456,7 @@ static moe_status dispatch_impl(moe_stage *st, int32_t slot, const moe_microbatc
         if (launch_gather_rows(mb->x, mb->x_scales, sl.slot_of_row,
                                sl.offsets + d.n_local_experts, d.top_k, d.d_model,
                                d.d_model / 128, sl.x_perm, sl.x_perm_s, (int32_t)st->sz.cap,
-                               (int32_t)max_rows, st->num_cus, s) != hipSuccess)
+                               (int32_t)max_rows, stream_cus(st, s), s) != hipSuccess)
             return MOE_EHIP;
         if (fp8 && d.has_shared_expert &&
             launch_transpose_scales(mb->x_scales, T, d.d_model / 128, sl.xsh_s, d.max_tokens,
@@ -514,24 +531,25 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     // bf16: groups of at most kSmallRows rows run in the small-group kernel,
     // the others in the 256x256-tile kernel (either may find no tiles).
     const int gmax = (int)st->sz.G;
+    const int cus = stream_cus(st, s);
     {
         ProfScope ps(st, 2, s);
         if (fp8) {
-            e = launch_gemm_fp8(g1, true, mt, gmax, st->num_cus, cap, tmax, s);
+            e = launch_gemm_fp8(g1, true, mt, gmax, cus, cap, tmax, s);
         } else {
-            e = launch_gemm_bf16_small(g1, true, gmax, st->num_cus, s);
-            if (e == hipSuccess) e = launch_gemm_bf16(g1, true, mt, st->num_cus, s);
+            e = launch_gemm_bf16_small(g1, true, gmax, cus, s);
+            if (e == hipSuccess) e = launch_gemm_bf16(g1, true, mt, cus, s);
         }
     }
     if (e == hipSuccess) {
         ProfScope ps(st, 3, s);
         if (fp8) {
-            e = launch_gemm_fp8(g2, false, mt, gmax, st->num_cus, cap, tmax, s);
+            e = launch_gemm_fp8(g2, false, mt, gmax, cus, cap, tmax, s);
         } else {
             // the down product (K = f) keeps 256x256 tiles for every group:
             // at ~130 rows its 28 column tiles per expert already fill the GPU
             g2.large_all = 1;
-            e = launch_gemm_bf16(g2, false, mt, st->num_cus, s);
+            e = launch_gemm_bf16(g2, false, mt, cus, s);
         }
     }
     if (e == hipErrorNotSupported) return MOE_EUNSUPPORTED;
@@ -558,7 +576,7 @@ static moe_status combine_impl(moe_stage *st, int32_t slot, void *stream, bool r
     c.accumulate = sl.mb.combine_mode == MOE_COMBINE_ACCUMULATE;
     {
         ProfScope ps(st, 4, s);
-        if (launch_combine(c, st->num_cus, s) != hipSuccess) return MOE_EHIP;
+        if (launch_combine(c, stream_cus(st, s), s) != hipSuccess) return MOE_EHIP;
     }
     return rec ? record(sl, s) : MOE_OK;
 }
