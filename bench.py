@@ -384,6 +384,97 @@ def run_triple_stream(name="c1", in_flight=3, steps=40, warmup=30, repeats=3):
             "ms_per_microbatch": round(best, 4), "tokens_per_s": round(T / (best / 1e3), 1)}
 
 
+def run_ingest(name="c1", senders=4, rounds=20, warmup=5):
+    """Asynchronous ingest (section 3.2.1): each round, `senders` senders copy
+    their share of a micro-batch (token rows, ids, weights) into the stage's
+    receive buffers and raise their ready words; the stage round waits for
+    them, runs, and acknowledges, and the next round's senders wait for that
+    acknowledgement before overwriting the buffers.
+      device-gated: both waits happen on the device (moe_ingest_wait /
+        moe_ingest_signal); the host enqueues every round without blocking;
+      host-gated: the host learns of each step's completion by synchronising
+        on an event before it enqueues the next.
+    Returns ms per round for both and their difference."""
+    import torch
+    from paper_2606_22541_amd import inputs
+    from paper_2606_22541_amd import moe_stage as C
+    from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
+
+    cfg = inputs.CONFIGS[name]
+    w = inputs.make_weights(cfg, "cuda")
+    mb = inputs.make_microbatches(cfg, "cuda")[0]
+    T = mb.ids.shape[0]
+    per = T // senders
+    sids, sw = to_device_routing(mb.ids, mb.w)
+    x = torch.empty_like(mb.x)                 # receive buffers
+    ids = torch.empty_like(sids)
+    wt = torch.empty_like(sw)
+    out = torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda")
+    ready = torch.zeros(senders, dtype=torch.int32, device="cuda")
+    consumed = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stage = ExpertStage(cfg, w, n_slots=2, max_tokens=T)
+    del w
+    m = stage.microbatch(x, ids, wt, out)
+    prod, cons, main = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    epoch = [0]
+
+    def send(r):
+        with torch.cuda.stream(prod):
+            for g in range(senders):
+                sl = slice(g * per, (g + 1) * per)
+                x[sl].copy_(mb.x[sl], non_blocking=True)
+                ids[sl].copy_(sids[sl], non_blocking=True)
+                wt[sl].copy_(sw[sl], non_blocking=True)
+                C.moe_ingest_signal(ready[g:g + 1], r, prod)
+
+    def device_gated(n):
+        for _ in range(n):
+            r = epoch[0] = epoch[0] + 1
+            C.moe_ingest_wait(stage.handle, consumed, 1, r - 1, 0, prod)
+            send(r)
+            C.moe_ingest_wait(stage.handle, ready, senders, r, 0, cons)
+            stage.submit(m, cons)
+            C.moe_ingest_signal(consumed, r, cons)
+
+    def host_gated(n):
+        for _ in range(n):
+            r = epoch[0] = epoch[0] + 1
+            send(r)
+            e = torch.cuda.Event()
+            e.record(prod)
+            e.synchronize()                    # the host learns the rows have arrived
+            stage.submit(m, cons)
+            C.moe_ingest_signal(consumed, r, cons)
+            e2 = torch.cuda.Event()
+            e2.record(cons)
+            e2.synchronize()                   # ... and that the buffers are free again
+
+    res = {}
+    for label, fn in (("device_gated", device_gated), ("host_gated", host_gated)):
+        fn(warmup)
+        stage.sync()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(main)
+        prod.wait_stream(main)
+        cons.wait_stream(main)
+        fn(rounds)
+        main.wait_stream(cons)
+        t1.record(main)
+        stage.sync()
+        torch.cuda.synchronize()
+        res[label] = t0.elapsed_time(t1) / rounds
+    stage.sync()
+    stage.close()
+    return {"workload": "%s micro-batch (T=%d) from %d senders of %d tokens through one set of "
+                        "receive buffers, %d rounds" % (name, T, senders, per, rounds),
+            "ms_per_round_device_gated": round(res["device_gated"], 4),
+            "ms_per_round_host_gated": round(res["host_gated"], 4),
+            "host_gating_us_per_round": round((res["host_gated"] - res["device_gated"]) * 1e3, 1)}
+
+
 SWEEP_TOKENS = (512, 1024, 2048, 4096, 8192, 12288, 16384, 24576, 32768)
 
 
@@ -555,6 +646,8 @@ def main():
                          "on separate streams (<= 1: skip)")
     ap.add_argument("--triple-stream", type=int, default=1,
                     help="also time the dispatch / GEMM / combine three-stream layout (0: skip)")
+    ap.add_argument("--ingest", type=int, default=1,
+                    help="also time device-gated against host-gated ingest (0: skip)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the latency-vs-tokens sweep of the c1 expert share")
     ap.add_argument("--layers", type=int, default=8,
@@ -622,6 +715,9 @@ def main():
     if args.triple_stream:
         line["%s_triple_stream" % args.workload] = run_triple_stream(args.workload)
         _log("[bench] triple-stream %s done" % args.workload)
+    if args.ingest:
+        line["%s_ingest" % args.workload] = run_ingest(args.workload)
+        _log("[bench] ingest %s done" % args.workload)
     if not args.no_sweep:
         line["token_sweep"] = run_sweep()
         _log("[bench] token sweep done")

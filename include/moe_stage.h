@@ -84,6 +84,7 @@ typedef int32_t moe_status;
 #define MOE_EUNSUPPORTED   (-5)   /* shape or mode this build does not support */
 #define MOE_EBUSY          (-6)   /* slot still in flight (non-blocking query) */
 #define MOE_EBADLAYER      (-7)   /* device saw a layer id outside [0, n_layers) */
+#define MOE_ETIMEOUT       (-8)   /* an ingest wait gave up (moe_ingest_wait) */
 
 enum { MOE_DTYPE_BF16 = 0, MOE_DTYPE_FP8_E4M3_B128 = 1 };
 enum { MOE_COMBINE_OVERWRITE = 0, MOE_COMBINE_ACCUMULATE = 1 };
@@ -204,13 +205,37 @@ MOE_API moe_status moe_stage_submit_microbatch(moe_stage *stage, const moe_micro
 MOE_API moe_status moe_quantize_fp8(const void *x_bf16, int32_t n_tokens, int32_t d_model,
                             void *x_q, float *x_s, void *stream);
 
+/* Asynchronous ingest (section 3.2.1; the per-sender ready bits of Table 2).
+ * The senders of a micro-batch write their token rows, ids and weights into
+ * receive buffers that live as long as the stage (the moe_microbatch
+ * pointers), then each raises its ready word with moe_ingest_signal.
+ * moe_ingest_wait enqueues on `stream` a wait, on the device, until every
+ * ready[i], i < n_words, has reached `epoch` (compared as a wrapping 32-bit
+ * round counter, so the words never need clearing); work enqueued on
+ * `stream` after it -- typically moe_stage_submit_microbatch, enqueued long
+ * before the rows arrive -- starts as soon as they have, with no host round
+ * trip.  The wait runs as one wave polling the words and is bounded: after
+ * spin_limit polls (0: about one second) it gives up, the work after it runs
+ * on whatever the buffers hold, and the next moe_stage_sync (once that work
+ * has been waited for) returns MOE_ETIMEOUT.  ready: device memory,
+ * 1 <= n_words <= 4096. */
+MOE_API moe_status moe_ingest_wait(moe_stage *stage, const uint32_t *ready, int32_t n_words,
+                           uint32_t epoch, uint32_t spin_limit, void *stream);
+
+/* Enqueues on `stream`, after its earlier work, a store of `epoch` into the
+ * device word *word with release order: a sender raising its ready word once
+ * its rows are written, or the MoE side acknowledging a consumed round so the
+ * senders may overwrite the buffers (backpressure). */
+MOE_API moe_status moe_ingest_signal(uint32_t *word, uint32_t epoch, void *stream);
+
 /* Fills `out` with the device pointers of `slot`'s workspace. */
 MOE_API moe_status moe_stage_query(moe_stage *stage, int32_t slot, moe_dispatch_view *out);
 
 /* Waits until every slot's enqueued work has completed and returns (then
  * clears) the sticky device errors: MOE_EBADID if a kernel saw an invalid
  * expert id since the last sync, else MOE_EBADLAYER if one saw an invalid
- * layer id, else MOE_OK (or MOE_EHIP). */
+ * layer id, else MOE_ETIMEOUT if an ingest wait gave up, else MOE_OK (or
+ * MOE_EHIP). */
 MOE_API moe_status moe_stage_sync(moe_stage *stage);
 
 /* Per-kernel timing with HIP events, for measurement (off by default).

@@ -19,6 +19,8 @@ constexpr int kDispatchChunk = 2048;            // 8 slots per thread
 constexpr int kMaxExperts = 1024;               // LDS histogram size
 constexpr int kMaxLocalExperts = 256;
 constexpr int kMaxLayers = 1024;
+constexpr int kMaxIngestWords = 4096;            // ready words one ingest wait may poll
+constexpr uint32_t kDefaultIngestSpins = 1u << 19;   // about a second of polling
 
 // Grouped GEMM tile: 256 x 256 output, K step 64 bf16 (or 128 e4m3) = 128 B
 // per row.
@@ -28,6 +30,7 @@ constexpr int kBN = 256;
 // Sticky error bits.
 constexpr int kErrBadId = 1;
 constexpr int kErrBadLayer = 2;
+constexpr int kErrIngestTimeout = 4;
 
 // Groups with at most this many rows ("small": a DeepSeek EP32 share at
 // T=4096 has ~128 rows per expert) take one full-height tile in the bf16

@@ -134,6 +134,14 @@ hipError_t launch_quantize_fp8(const void *x, int32_t n_rows, const int32_t *n_r
                                int32_t d, void *xq, float *xs, int32_t scale_ld, int num_cus,
                                hipStream_t s);
 
+// Asynchronous ingest: a bounded device-side wait until every ready[i]
+// (i < n_words) has reached `epoch` (wrapping compare); after spin_limit
+// polls it gives up and sets kErrIngestTimeout in err.  signal: a release
+// store of `epoch` into *word after the stream's earlier work.
+hipError_t launch_ingest_wait(const uint32_t *ready, int32_t n_words, uint32_t epoch,
+                              uint32_t spin_limit, int32_t *err, hipStream_t s);
+hipError_t launch_ingest_signal(uint32_t *word, uint32_t epoch, hipStream_t s);
+
 // Weight packing at create time.  Gate and up rows are interleaved in
 // blocks of `interleave` rows: packed row 2*il*b + i is gate row il*b + i for
 // i < il and up row il*b + (i - il) otherwise.  bf16 uses il = 16 (a 32-column

@@ -270,6 +270,7 @@ const char *moe_status_string(moe_status s)
     case MOE_EUNSUPPORTED: return "unsupported shape or mode";
     case MOE_EBUSY: return "slot busy";
     case MOE_EBADLAYER: return "layer id outside [0, n_layers) seen on the device (clamped)";
+    case MOE_ETIMEOUT: return "an ingest wait gave up before every ready word reached its epoch";
     default: return "unknown status";
     }
 }
@@ -681,6 +682,22 @@ moe_status moe_stage_profile_read(moe_stage *st, double *ms, int32_t *launches)
     return r;
 }
 
+moe_status moe_ingest_wait(moe_stage *st, const uint32_t *ready, int32_t n_words, uint32_t epoch,
+                           uint32_t spin_limit, void *stream)
+{
+    if (!st || !ready || n_words < 1 || n_words > kMaxIngestWords) return MOE_EINVAL;
+    if (launch_ingest_wait(ready, n_words, epoch, spin_limit ? spin_limit : kDefaultIngestSpins,
+                           st->err, (hipStream_t)stream) != hipSuccess)
+        return MOE_EHIP;
+    return MOE_OK;
+}
+
+moe_status moe_ingest_signal(uint32_t *word, uint32_t epoch, void *stream)
+{
+    if (!word) return MOE_EINVAL;
+    return launch_ingest_signal(word, epoch, (hipStream_t)stream) == hipSuccess ? MOE_OK : MOE_EHIP;
+}
+
 moe_status moe_stage_sync(moe_stage *st)
 {
     if (!st) return MOE_EINVAL;
@@ -694,7 +711,7 @@ moe_status moe_stage_sync(moe_stage *st)
         if (hipMemsetAsync(st->err, 0, 4, st->own) != hipSuccess ||
             hipStreamSynchronize(st->own) != hipSuccess)
             return MOE_EHIP;
-        return (err & kErrBadId) ? MOE_EBADID : MOE_EBADLAYER;
+        return (err & kErrBadId) ? MOE_EBADID : (err & kErrBadLayer) ? MOE_EBADLAYER : MOE_ETIMEOUT;
     }
     return MOE_OK;
 }

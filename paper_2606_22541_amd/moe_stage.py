@@ -26,6 +26,7 @@ MOE_EBADID = -4
 MOE_EUNSUPPORTED = -5
 MOE_EBUSY = -6
 MOE_EBADLAYER = -7
+MOE_ETIMEOUT = -8
 MOE_DTYPE_BF16 = 0
 MOE_DTYPE_FP8_E4M3_B128 = 1
 MOE_COMBINE_OVERWRITE = 0
@@ -36,7 +37,7 @@ EXPORTS = (
     "moe_stage_create", "moe_stage_destroy", "moe_dispatch", "moe_expert_ffn", "moe_combine",
     "moe_stage_submit_microbatch", "moe_quantize_fp8", "moe_stage_query", "moe_stage_sync",
     "moe_stage_workspace_bytes", "moe_status_string", "moe_stage_profile",
-    "moe_stage_profile_read",
+    "moe_stage_profile_read", "moe_ingest_wait", "moe_ingest_signal",
 )
 MOE_PROF_KINDS = 6
 PROF_KIND_NAMES = ("dispatch_index", "gather", "gemm_gate_up_swiglu", "gemm_down", "combine",
@@ -106,6 +107,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "moe_stage_profile": (st, [P, ctypes.c_int32]),
         "moe_stage_profile_read": (st, [P, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int32)]),
+        "moe_ingest_wait": (st, [P, P, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint32, P]),
+        "moe_ingest_signal": (st, [P, ctypes.c_uint32, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -241,3 +244,15 @@ def moe_stage_profile_read(stage: int):
     n = (ctypes.c_int32 * MOE_PROF_KINDS)()
     _check(load_library().moe_stage_profile_read(stage, ms, n), "moe_stage_profile_read")
     return {PROF_KIND_NAMES[i]: (ms[i], n[i]) for i in range(MOE_PROF_KINDS)}
+
+
+def moe_ingest_wait(stage: int, ready, n_words: int, epoch: int, spin_limit: int = 0,
+                    stream=None) -> None:
+    _check(load_library().moe_ingest_wait(stage, _ptr(ready), int(n_words), epoch & 0xFFFFFFFF,
+                                          int(spin_limit), _stream(stream)), "moe_ingest_wait")
+
+
+def moe_ingest_signal(word, epoch: int, stream=None) -> None:
+    _check(load_library().moe_ingest_signal(_ptr(word), epoch & 0xFFFFFFFF, _stream(stream)),
+           "moe_ingest_signal")
+

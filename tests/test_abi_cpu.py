@@ -43,7 +43,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 def test_status_strings(lib):
     for code in (C.MOE_OK, C.MOE_EINVAL, C.MOE_ENOMEM, C.MOE_EHIP, C.MOE_EBADID,
-                 C.MOE_EUNSUPPORTED, C.MOE_EBUSY, C.MOE_EBADLAYER):
+                 C.MOE_EUNSUPPORTED, C.MOE_EBUSY, C.MOE_EBADLAYER, C.MOE_ETIMEOUT):
         assert C.moe_status_string(code) not in ("", "unknown status")
     assert C.moe_status_string(12345) == "unknown status"
 
@@ -107,6 +107,8 @@ def test_invalid_desc_rejected(lib, bad):
 
 
 def test_null_arguments_rejected_without_gpu(lib):
+    assert lib.moe_ingest_wait(None, None, 1, 1, 0, None) == C.MOE_EINVAL
+    assert lib.moe_ingest_signal(None, 1, None) == C.MOE_EINVAL
     assert lib.moe_stage_sync(None) == C.MOE_EINVAL
     assert lib.moe_dispatch(None, 0, None, None) == C.MOE_EINVAL
     assert lib.moe_stage_create(None, None, None) == C.MOE_EINVAL
