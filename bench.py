@@ -697,6 +697,11 @@ def main():
         "kernels": stream_rooflines(prim),
     }
     _log("[bench] primary done: %.3f ms/step" % ms_step)
+    # before the multi-stream workloads: their streams would share hardware
+    # queues with the ingest measurement's sender and stage streams
+    if args.ingest:
+        line["%s_ingest" % args.workload] = run_ingest(args.workload)
+        _log("[bench] ingest %s done" % args.workload)
     for name in [n for n in args.secondary.split(",") if n]:
         sec = run_workload(name, max(args.steps // 2, 5), args.warmup)
         line[name] = {
@@ -715,9 +720,6 @@ def main():
     if args.triple_stream:
         line["%s_triple_stream" % args.workload] = run_triple_stream(args.workload)
         _log("[bench] triple-stream %s done" % args.workload)
-    if args.ingest:
-        line["%s_ingest" % args.workload] = run_ingest(args.workload)
-        _log("[bench] ingest %s done" % args.workload)
     if not args.no_sweep:
         line["token_sweep"] = run_sweep()
         _log("[bench] token sweep done")

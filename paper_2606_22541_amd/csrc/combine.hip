@@ -87,7 +87,10 @@ void k_combine(const uint4 *__restrict__ y, const uint4 *__restrict__ ysh,
                     bf16 *ob = (bf16 *)&o;
 #pragma unroll
                     for (int i = 0; i < 8; ++i) ob[i] = f2bf(acc[u][i]);
-                    orow[c] = o;
+                    // the output is not read again by the stage: stream it to
+                    // HBM now rather than leave dirty lines for the next
+                    // micro-batch's weight stream to evict
+                    __builtin_nontemporal_store(*(const u32x4 *)&o, (u32x4 *)&orow[c]);
                 }
             }
         }
