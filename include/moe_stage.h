@@ -92,7 +92,8 @@ enum { MOE_COMBINE_OVERWRITE = 0, MOE_COMBINE_ACCUMULATE = 1 };
 /* Stage shape.  Requirements: d_model and d_ff multiples of 128;
  * 1 <= n_experts <= 1024; 0 <= first_local_expert;
  * 1 <= n_local_experts <= 256; first_local_expert + n_local_experts <=
- * n_experts; 1 <= top_k <= 32; 0 <= max_tokens; 1 <= n_slots <= 64;
+ * n_experts; 1 <= top_k <= 32; 0 <= max_tokens with max_tokens * d_model * 2
+ * < 2^31 (token rows are addressed with 32-bit offsets); 1 <= n_slots <= 64;
  * 1 <= n_layers <= 1024 (every layer has the same shape and local experts). */
 typedef struct {
     int32_t d_model;             /* hidden size d (paper: H) */

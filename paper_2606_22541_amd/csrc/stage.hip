@@ -64,6 +64,8 @@ bool desc_ok(const moe_stage_desc *d)
     if ((int64_t)d->max_tokens * d->top_k >= (int64_t)1 << 31) return false;
     if ((int64_t)256 * d->d_model * 2 >= (int64_t)1 << 31) return false;
     if ((int64_t)256 * d->d_ff * 2 >= (int64_t)1 << 31) return false;
+    // the bf16 gate/up GEMM addresses token rows of x with 32-bit byte offsets
+    if ((int64_t)d->max_tokens * d->d_model * 2 >= (int64_t)1 << 31) return false;
     return true;
 }
 

@@ -95,6 +95,7 @@ def test_workspace_bytes_scale_with_layers(lib):
     dict(n_local_experts=0), dict(first_local_expert=250), dict(top_k=0), dict(top_k=33),
     dict(max_tokens=-1), dict(n_slots=0), dict(dtype=7), dict(has_shared_expert=2),
     dict(n_layers=0), dict(n_layers=-3), dict(n_layers=1025),
+    dict(d_model=7168, max_tokens=150000),              # token rows past 32-bit offsets
 ])
 def test_invalid_desc_rejected(lib, bad):
     args = dict(d_model=256, d_ff=128, n_experts=8, first_local_expert=0, n_local_experts=4,
