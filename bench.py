@@ -543,8 +543,10 @@ def run_layers(n_layers, passes=3):
         next by reading the id back from the device (which waits for the
         stream), then enqueues it -- the dispatch pattern whose per-layer
         latency the super kernel removes.
-    Returns ms per layer for both and their difference (the per-layer host
-    dispatch bubble)."""
+    Returns ms per layer for both and the GPU's idle time between one layer's
+    end and the next layer's start (events around each submission); their
+    difference is the per-layer host dispatch bubble.  (Per-layer times also
+    differ through caching: idle gaps let earlier writes drain.)"""
     import torch
     from paper_2606_22541_amd import inputs
     from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
@@ -564,30 +566,40 @@ def run_layers(n_layers, passes=3):
     main = torch.cuda.Stream()
     torch.cuda.synchronize()
 
-    def device_resolved():
+    def device_resolved(marks):
         for m in mbs:
+            a = torch.cuda.Event(enable_timing=True)
+            a.record(main)
             stage.submit(m, main)
+            b = torch.cuda.Event(enable_timing=True)
+            b.record(main)
+            marks.append((a, b))
 
-    def host_dispatched():
+    def host_dispatched(marks):
         for i, m in enumerate(mbs):
             with torch.cuda.stream(main):
                 assert int(lids[i].item()) == order[i]   # synchronising read of the layer id
+            a = torch.cuda.Event(enable_timing=True)
+            a.record(main)
             stage.submit(m, main)
+            b = torch.cuda.Event(enable_timing=True)
+            b.record(main)
+            marks.append((a, b))
 
-    res = {}
+    res, gaps = {}, {}
     for name, fn in (("device_resolved", device_resolved), ("host_dispatched", host_dispatched)):
-        fn()                                           # warm-up pass
+        fn([])                                         # warm-up pass
         stage.sync()
         torch.cuda.synchronize()
-        start = torch.cuda.Event(enable_timing=True)
-        end = torch.cuda.Event(enable_timing=True)
-        start.record(main)
+        marks = []
         for _ in range(passes):
-            fn()
-        end.record(main)
+            fn(marks)
         stage.sync()
         torch.cuda.synchronize()
-        res[name] = start.elapsed_time(end) / (passes * n_layers)
+        res[name] = (marks[0][0].elapsed_time(marks[-1][1])) / len(marks)
+        # GPU idle time between one layer's end and the next layer's start
+        g = [marks[i][1].elapsed_time(marks[i + 1][0]) for i in range(len(marks) - 1)]
+        gaps[name] = float(np.mean(g)) * 1e3
     stage.close()
     return {
         "layers": n_layers,
@@ -595,7 +607,9 @@ def run_layers(n_layers, passes=3):
                     "bf16) x %d layers resident, layers in shuffled order" % n_layers,
         "ms_per_layer_device_resolved": round(res["device_resolved"], 4),
         "ms_per_layer_host_dispatched": round(res["host_dispatched"], 4),
-        "host_bubble_us_per_layer": round((res["host_dispatched"] - res["device_resolved"]) * 1e3, 1),
+        "gap_us_between_layers_device_resolved": round(gaps["device_resolved"], 1),
+        "gap_us_between_layers_host_dispatched": round(gaps["host_dispatched"], 1),
+        "host_bubble_us_per_layer": round(gaps["host_dispatched"] - gaps["device_resolved"], 1),
     }
 
 
