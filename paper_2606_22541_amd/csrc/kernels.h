@@ -77,6 +77,18 @@ struct GemmArgs {
     int32_t *err;
 };
 
+// A pointer loaded from memory, made provably wave-uniform (the value is the
+// same in every lane), so that buffer descriptors built from it stay in
+// scalar registers instead of being re-established lane by lane at each load.
+template <typename T>
+__device__ __forceinline__ T *uniform_ptr(T *p)
+{
+    const uint64_t v = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (T *)(((uint64_t)hi << 32) | lo);
+}
+
 // The weights a GEMM launch uses: a.B / a.Bs, or the ones of the layer named
 // in device memory (read once per workgroup; every wave gets the same value).
 __device__ __forceinline__ void resolve_weights(const GemmArgs &a, const void *&B, const float *&Bs)
@@ -90,8 +102,8 @@ __device__ __forceinline__ void resolve_weights(const GemmArgs &a, const void *&
             l = l < 0 ? 0 : a.n_layers - 1;
         }
         const LayerWeights &lw = a.layers[l];
-        B = a.down ? lw.w2 : lw.w1;
-        Bs = a.down ? lw.s2 : lw.s1;
+        B = uniform_ptr(a.down ? lw.w2 : lw.w1);
+        Bs = uniform_ptr(a.down ? lw.s2 : lw.s1);
     }
 }
 
