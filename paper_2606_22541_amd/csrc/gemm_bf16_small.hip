@@ -150,10 +150,19 @@ __device__ __forceinline__ void small_step(const SmallTile &t, const SmallLds &l
 
 // One tile with NMB 32-row blocks: K loop, K-half reduction and epilogue,
 // fully unrolled over the row blocks so no accumulator crosses a branch.
+// K-half partials of column half ch: block q = 2 mb + cb (16 x 64 floats,
+// 4 KB) lives in ring buffer 2 ch + q / 6 at 4 KB (q % 6).  Callers pass q
+// from fully unrolled loops, so it folds to a base plus an immediate.
+__device__ __forceinline__ float *partial_block(const SmallLds &l, int ch, int q)
+{
+    return (float *)(ch ? l.a[2 + q / 6] : l.a[q / 6]) + (q % 6) * 16 * 64;
+}
+
 template <bool SWIGLU, int NMB>
 __device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLds &l,
-                                               const SmallWave &w, float *red)
+                                               const SmallWave &w)
 {
+    static_assert(2 * NMB <= 12, "two 24 KB ring buffers per column half");
     f32x16 acc[NMB][2];
 #pragma unroll
     for (int i = 0; i < NMB; ++i) acc[i][0] = acc[i][1] = (f32x16){};
@@ -177,15 +186,15 @@ __device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLd
     __syncthreads();   // all ring reads done: the ring now holds the K-half partials
 
     // wave (1, ch) hands its partial sums to wave (0, ch), lane-contiguous
-    float *part = red + w.ch * (NMB * 2 * 16 * 64);
     if (w.kh == 1) {
 #pragma unroll
         for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb)
+            for (int cb = 0; cb < 2; ++cb) {
+                float *part = partial_block(l, w.ch, mb * 2 + cb) + w.lane;
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    part[((mb * 2 + cb) * 16 + r) * 64 + w.lane] = acc[mb][cb][r];
+                for (int r = 0; r < 16; ++r) part[r * 64] = acc[mb][cb][r];
+            }
     }
     __syncthreads();
     if (w.kh == 0) {
@@ -197,8 +206,9 @@ __device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLd
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
                 f32x16 v = acc[mb][cb];
+                const float *part = partial_block(l, w.ch, mb * 2 + cb) + w.lane;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) v[r] += part[((mb * 2 + cb) * 16 + r) * 64 + w.lane];
+                for (int r = 0; r < 16; ++r) v[r] += part[r * 64];
                 const int cbase = t.n0 + w.ch * 64 + cb * 32;
                 if constexpr (SWIGLU) {
                     const int f = t.N / 2;
@@ -236,8 +246,8 @@ void k_gemm_bf16_small(GemmArgs a)
     __shared__ __attribute__((aligned(1024))) bf16 lds_a3[kSmallRows * kRowEs];
     const SmallLds l{{lds_a0, lds_a1, lds_a2, lds_a3}};
     // K-half partials after the K loop: 2 x (6 x 2 x 16 x 64) floats = 96 KB,
-    // which is exactly the ring; the four buffers are declared back to back.
-    static_assert(2 * 6 * 2 * 16 * 64 * 4 == 4 * kSmallRows * kRowEs * 2, "partials = ring");
+    // the ring's four buffers, each holding six 4 KB partial blocks.
+    static_assert(6 * 16 * 64 * 4 == kSmallRows * kRowEs * 2, "six partial blocks per ring buffer");
 
     const int tid = threadIdx.x;
     SmallWave w;
@@ -290,14 +300,13 @@ void k_gemm_bf16_small(GemmArgs a)
                                           K * 2, w.lane);
         t.rb = rsrc_s(B, (int64_t)min(kTNs, N - t.n0) * K * 2);
         t.C = (bf16 *)(sh ? a.C_shared : a.C_routed);
-        float *red = (float *)lds_a0;
         switch ((t.rows_valid + 31) >> 5) {   // 32-row blocks holding rows: 1..6
-        case 1: run_small_tile<SWIGLU, 1>(t, l, w, red); break;
-        case 2: run_small_tile<SWIGLU, 2>(t, l, w, red); break;
-        case 3: run_small_tile<SWIGLU, 3>(t, l, w, red); break;
-        case 4: run_small_tile<SWIGLU, 4>(t, l, w, red); break;
-        case 5: run_small_tile<SWIGLU, 5>(t, l, w, red); break;
-        default: run_small_tile<SWIGLU, 6>(t, l, w, red); break;
+        case 1: run_small_tile<SWIGLU, 1>(t, l, w); break;
+        case 2: run_small_tile<SWIGLU, 2>(t, l, w); break;
+        case 3: run_small_tile<SWIGLU, 3>(t, l, w); break;
+        case 4: run_small_tile<SWIGLU, 4>(t, l, w); break;
+        case 5: run_small_tile<SWIGLU, 5>(t, l, w); break;
+        default: run_small_tile<SWIGLU, 6>(t, l, w); break;
         }
     }
 }
