@@ -46,6 +46,14 @@ struct GroupTable {
     int32_t *mt_base;   // [G+1] prefix of ceil(rows / kBM) over all groups
     int32_t *lt_base;   // [G+1] same, counting only groups with rows > kSmallRows
     int32_t *st_base;   // [G+1] prefix of 1 per group with 1 <= rows <= kSmallRows
+    // Tile order of the 256-row bf16 GEMM: the full row tiles of every group
+    // first, then the partial ones (rows % kBM != 0), largest first, so the
+    // cheap partial tiles fill the last round of the persistent grid.
+    int32_t *fm_base;   // [G+1] prefix of rows / kBM over all groups
+    int32_t *fl_base;   // [G+1] same, over groups with rows > kSmallRows
+    int32_t *pm_list;   // [G+1] groups with a partial row tile, by descending
+                        //       rows % kBM (ties: lower index first); count at [G]
+    int32_t *pl_list;   // [G+1] same, over groups with rows > kSmallRows
 };
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }

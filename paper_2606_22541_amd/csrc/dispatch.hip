@@ -76,6 +76,85 @@ void k_hist(const int32_t *__restrict__ ids, int32_t n_slots, int32_t E,
         blk_counts[(int64_t)blockIdx.x * E + x] = h[x];
 }
 
+// Exclusive prefix sum over the 64 lanes of a wave; *total receives the sum.
+__device__ __forceinline__ int wave_excl_scan(int v, int lane, int &total)
+{
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    total = __shfl(x, 63);
+    return x - v;
+}
+
+// Grouped-GEMM tile tables over G = E_loc (+1 shared) groups (GroupTable),
+// built by one wave in chunks of 64 groups with shuffle scans, so no
+// workgroup barrier sits in the dispatch for them.  rows[i] is the local
+// expert's token count (tot), or T for the shared expert.
+__device__ void build_group_tables(const GroupTable &g, const int32_t *tot, int E_loc,
+                                   int has_shared, int T, int lane)
+{
+    const int G = E_loc + (has_shared ? 1 : 0);
+    int c_row = 0, c_mt = 0, c_lt = 0, c_st = 0, c_fm = 0, c_fl = 0, c_pm = 0, c_pl = 0;
+    for (int c0 = 0; c0 < G; c0 += 64) {
+        const int i = c0 + lane;
+        const int rows = i < E_loc ? tot[i] : (i < G ? T : 0);
+        const int m = (rows + kBM - 1) / kBM;
+        const bool large = rows > kSmallRows;
+        const int fm = rows / kBM, rem = rows - fm * kBM;
+        int t_row, t_mt, t_lt, t_st, t_fm, t_fl, t_pm, t_pl;
+        const int p_row = wave_excl_scan(i < E_loc ? rows : 0, lane, t_row);
+        const int p_mt = wave_excl_scan(m, lane, t_mt);
+        const int p_lt = wave_excl_scan(large ? m : 0, lane, t_lt);
+        const int p_st = wave_excl_scan(rows > 0 && !large ? 1 : 0, lane, t_st);
+        const int p_fm = wave_excl_scan(fm, lane, t_fm);
+        const int p_fl = wave_excl_scan(large ? fm : 0, lane, t_fl);
+        wave_excl_scan(rem > 0 ? 1 : 0, lane, t_pm);
+        wave_excl_scan(rem > 0 && large ? 1 : 0, lane, t_pl);
+        if (i < G) {
+            g.row0[i] = i < E_loc ? c_row + p_row : 0;
+            g.rows[i] = rows;
+            g.mt_base[i] = c_mt + p_mt;
+            g.lt_base[i] = c_lt + p_lt;
+            g.st_base[i] = c_st + p_st;
+            g.fm_base[i] = c_fm + p_fm;
+            g.fl_base[i] = c_fl + p_fl;
+            if (rem > 0) {
+                // rank among the partial row tiles: more rows first, then lower index
+                int rank_m = 0, rank_l = 0;
+                for (int j = 0; j < G; ++j) {
+                    const int rj = j < E_loc ? tot[j] : T;
+                    const int qj = rj % kBM;
+                    const bool before = qj > 0 && (qj > rem || (qj == rem && j < i));
+                    rank_m += before ? 1 : 0;
+                    rank_l += (before && rj > kSmallRows) ? 1 : 0;
+                }
+                g.pm_list[rank_m] = i;
+                if (large) g.pl_list[rank_l] = i;
+            }
+        }
+        c_row += t_row;
+        c_mt += t_mt;
+        c_lt += t_lt;
+        c_st += t_st;
+        c_fm += t_fm;
+        c_fl += t_fl;
+        c_pm += t_pm;
+        c_pl += t_pl;
+    }
+    if (lane == 0) {
+        g.mt_base[G] = c_mt;
+        g.lt_base[G] = c_lt;
+        g.st_base[G] = c_st;
+        g.fm_base[G] = c_fm;
+        g.fl_base[G] = c_fl;
+        g.pm_list[G] = c_pm;
+        g.pl_list[G] = c_pl;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // 2. Placement.  Workgroup b owns the same kDispatchChunk slots as histogram
 //    workgroup b; wave w owns slots [b*chunk + w*chunk/4, b*chunk +
@@ -173,35 +252,6 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
     if (b == 0) {
         if (tid < E_loc) offsets[tid] = off_i;
         if (tid == 0) offsets[E_loc] = total;
-        // tile tables over G = E_loc (+1 shared) groups, in chunks of 256
-        const int G = E_loc + (has_shared ? 1 : 0);
-        int c_mt = 0, c_lt = 0, c_st = 0;
-        for (int c0 = 0; c0 < G; c0 += kDispatchThreads) {
-            const int i = c0 + tid;
-            const int rows = i < E_loc ? tot[i] : (i < G ? T : 0);
-            const int m = (rows + kBM - 1) / kBM;
-            const int lt = rows > kSmallRows ? m : 0;
-            const int sm = (rows > 0 && rows <= kSmallRows) ? 1 : 0;
-            int t_mt, t_lt, t_st;
-            const int p_mt = block_excl_scan(m, wsum, t_mt);
-            const int p_lt = block_excl_scan(lt, wsum, t_lt);
-            const int p_st = block_excl_scan(sm, wsum, t_st);
-            if (i < G) {
-                g.row0[i] = i < E_loc ? off_i : 0;
-                g.rows[i] = rows;
-                g.mt_base[i] = c_mt + p_mt;
-                g.lt_base[i] = c_lt + p_lt;
-                g.st_base[i] = c_st + p_st;
-            }
-            c_mt += t_mt;
-            c_lt += t_lt;
-            c_st += t_st;
-        }
-        if (tid == 0) {
-            g.mt_base[G] = c_mt;
-            g.lt_base[G] = c_lt;
-            g.st_base[G] = c_st;
-        }
     }
     __syncthreads();
 
@@ -228,6 +278,9 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
             if (pos >= 0) slot_of_row[pos] = (int32_t)sl;
         }
     }
+    // after this wave's own placement, so the other waves and workgroups
+    // place their slots meanwhile
+    if (b == 0 && wave == 0) build_group_tables(g, tot, E_loc, has_shared, T, lane);
 }
 
 hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)

@@ -24,14 +24,27 @@
 //    ds_read_b128 hit 64 distinct banks; weight fragments arrive in MFMA
 //    fragment order (see launch_pack_frag_bf16), one contiguous 1 KB per
 //    load, and are read back lane-contiguous, also free of bank conflicts;
-//  * every step issues the same loads (steps past K re-read the last one),
-//    so the wait before each step is a constant and no wait drains the
-//    look-ahead;
+//  * every step of a wave issues the same loads (steps past K re-read the
+//    last one), so the wait before each step is a constant and no wait
+//    drains the look-ahead;
 //  * the raw buffer range check returns zeros for rows past the group's
 //    end, so ragged groups need no clamping;
+//  * in the size order below, a partial row tile (the last one of a group
+//    whose rows are not a multiple of 256) runs only the 32-row blocks that
+//    hold rows: each wave takes the instance of its K loop for its number of
+//    such blocks, and a wave whose 128-row half is empty loads no token rows
+//    and runs no MFMAs (it still fills its share of the weight fragments);
+//  * when the last round of the persistent grid would be at most half full,
+//    tiles are numbered full tiles first, then partial tiles in decreasing
+//    order of rows (tables built by the dispatch), so the cheaper partial
+//    tiles form that last round; otherwise the band order below is kept, in
+//    which a partial tile reads its weight panels from L2 beside the full
+//    tiles of its band, and no row blocks are skipped (skipping them there
+//    only shifts power to the other CUs without shortening the longest
+//    list of tiles);
 //  * the tile order is XCD-aware: workgroups are placed round-robin on the 8
 //    XCDs, so consecutive tile numbers are handed to the 32 workgroups of one
-//    XCD, and within a group tiles are rastered in bands of 4 row-tiles,
+//    XCD, and within a group (full) tiles are rastered in bands of 4 row-tiles,
 //    letting one XCD's L2 serve 4 row panels x 8 weight panels at a time;
 //  * SwiGLU mode fuses h = SiLU(gate) * up into the epilogue: the weight
 //    matrix packs gate and up rows in interleaved blocks of 16, so every
@@ -110,14 +123,17 @@ struct Stage {
 // offset, which the buffer range check covers (rows past the group read as
 // zero); the scalar offset, which it does not cover, only moves along K and
 // between weight column blocks that exist (absent ones re-read the last).
+template <bool AROWS>
 __device__ __forceinline__ void fill(const Tile &t, const WaveConst &w, const Stage &st, int j)
 {
     const int js = min(j, t.KT - 1);
+    if constexpr (AROWS) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            t.ra, (lds_void *)(st.a + (w.wave * 32 + i * 16) * kRowElems), 16,
-            i ? t.va1 : t.va0, js * kBK * 2, 0, 0);
+        for (int i = 0; i < 2; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                t.ra, (lds_void *)(st.a + (w.wave * 32 + i * 16) * kRowElems), 16,
+                i ? t.va1 : t.va0, js * kBK * 2, 0, 0);
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int f = w.wave * 2 + i;             // fragment of the stage: 2 cb + kk
@@ -130,43 +146,101 @@ __device__ __forceinline__ void fill(const Tile &t, const WaveConst &w, const St
 
 // One K step: wait for this step's stage, sync, refill the stage freed by
 // the previous step, then 2 sub-steps of 8 MFMAs.
-template <int S>
+template <int S, int NMB>
 __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const Stage (&ring)[4],
-                                      f32x16 (&acc)[4][2], int j)
+                                      f32x16 (&acc)[NMB > 0 ? NMB : 1][2], int j)
 {
     // The fills of steps j+1 and j+2 are the loads issued after step j's.
-    constexpr int kAfter = 2 * kFill;
+    constexpr int kAfter = 2 * (NMB > 0 ? 4 : 2);
     __builtin_amdgcn_s_waitcnt((kAfter & 15) | ((kAfter >> 4) << 14) | (7 << 4) | (15 << 8));
     __builtin_amdgcn_s_barrier();   // every wave's fill of step j landed; step j-1 read
-    fill(t, w, ring[(S + 3) & 3], j + 3);
+    fill<(NMB > 0)>(t, w, ring[(S + 3) & 3], j + 3);
     __builtin_amdgcn_sched_barrier(0);
-
-    const bf16 *As = ring[S].a;
-    const bf16 *Bs = ring[S].b;
-    auto read = [&](int kk, bf16x8 (&af)[4], bf16x8 (&bfr)[2]) {
-        const int ch = ((kk * 2 + w.rd_hi) ^ w.swz) << 3;
+    if constexpr (NMB > 0) {
+        const bf16 *As = ring[S].a;
+        const bf16 *Bs = ring[S].b;
+        auto read = [&](int kk, bf16x8 (&af)[NMB], bf16x8 (&bfr)[2]) {
+            const int ch = ((kk * 2 + w.rd_hi) ^ w.swz) << 3;
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
-            af[mb] = *(const bf16x8 *)&As[w.a_rd + mb * 32 * kRowElems + ch];
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-            bfr[nb] = *(const bf16x8 *)&Bs[w.b_rd + (nb * 2 + kk) * 512];
-    };
-    auto mma = [&](const bf16x8 (&af)[4], const bf16x8 (&bfr)[2]) {
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
+            for (int mb = 0; mb < NMB; ++mb)
+                af[mb] = *(const bf16x8 *)&As[w.a_rd + mb * 32 * kRowElems + ch];
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb)
-                acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb],
-                                                                     acc[mb][nb], 0, 0, 0);
-    };
-    bf16x8 a0[4], b0[2], a1[4], b1[2];
-    read(0, a0, b0);
-    read(1, a1, b1);
-    __builtin_amdgcn_sched_barrier(0);
-    mma(a0, b0);
-    mma(a1, b1);
-    __builtin_amdgcn_sched_barrier(0);
+                bfr[nb] = *(const bf16x8 *)&Bs[w.b_rd + (nb * 2 + kk) * 512];
+        };
+        auto mma = [&](const bf16x8 (&af)[NMB], const bf16x8 (&bfr)[2]) {
+#pragma unroll
+            for (int mb = 0; mb < NMB; ++mb)
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb)
+                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb],
+                                                                         acc[mb][nb], 0, 0, 0);
+        };
+        bf16x8 a0[NMB], b0[2], a1[NMB], b1[2];
+        read(0, a0, b0);
+        read(1, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(a0, b0);
+        mma(a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// One tile for a wave whose 128-row half holds NMB non-empty 32-row blocks:
+// K loop, then the epilogue.  NMB = 0 only for the upper half of a tile of
+// at most 128 rows: the wave then loads no token rows (they are all past the
+// group) and runs no MFMAs, but still fills its share of weight fragments.
+template <bool SWIGLU, int NMB>
+__device__ __forceinline__ void run_tile(const Tile &t, const WaveConst &w, const Stage (&ring)[4],
+                                         const GemmArgs &a, int N, int n0, int row0, int rows_valid,
+                                         bool sh, int wm, int wn, int lane)
+{
+    f32x16 acc[NMB > 0 ? NMB : 1][2];
+#pragma unroll
+    for (int i = 0; i < (NMB > 0 ? NMB : 1); ++i) acc[i][0] = acc[i][1] = (f32x16){};
+    fill<(NMB > 0)>(t, w, ring[0], 0);
+    fill<(NMB > 0)>(t, w, ring[1], 1);
+    fill<(NMB > 0)>(t, w, ring[2], 2);
+    // K is a multiple of 128, so KT is a multiple of 4.
+    for (int j = 0; j < t.KT; j += 4) {
+        kstep<0, NMB>(t, w, ring, acc, j);
+        kstep<1, NMB>(t, w, ring, acc, j + 1);
+        kstep<2, NMB>(t, w, ring, acc, j + 2);
+        kstep<3, NMB>(t, w, ring, acc, j + 3);
+    }
+    __syncthreads();   // drain the look-ahead fills before the ring is reused
+    if constexpr (NMB > 0) {
+        bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                const f32x16 v = acc[mb][nb];
+                const int rbase = wm * 128 + mb * 32 + w.rd_hi * 4;
+                if constexpr (SWIGLU) {
+                    const int f = N / 2;
+                    const bool gl = (lane & 16) == 0;
+                    const int hc = (n0 + wn * 64 + nb * 32) / 2 + (lane & 15);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const float up = __shfl_xor(v[r], 16);
+                        const int lr = rbase + (r >> 2) * 8 + (r & 3);
+                        if (gl && lr < rows_valid)
+                            C[(int64_t)(row0 + lr) * f + hc] =
+                                f2bf(v[r] / (1.0f + __expf(-v[r])) * up);
+                    }
+                } else {
+                    const int col = n0 + wn * 64 + nb * 32 + (lane & 31);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int lr = rbase + (r >> 2) * 8 + (r & 3);
+                        if (lr < rows_valid && col < N)
+                            C[(int64_t)(row0 + lr) * N + col] = f2bf(v[r]);
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+    }
 }
 
 }  // namespace
@@ -198,6 +272,15 @@ void k_gemm_bf16(GemmArgs a)
     const int32_t *tbase = a.large_all ? a.groups.mt_base : a.groups.lt_base;
     const int total = __builtin_amdgcn_readfirstlane(tbase[a.G] * NT);
     const int P = gridDim.x;
+    // A last round that fills at most half the grid is worth reordering:
+    // full tiles first, then the partial tiles largest first, each running
+    // only its non-empty row blocks.  Otherwise the band order keeps every
+    // partial tile next to the full tiles that share its weight panels in L2.
+    const int tail = total % P;
+    const bool by_size = tail != 0 && 2 * tail <= P;
+    const int32_t *fbase = a.large_all ? a.groups.fm_base : a.groups.fl_base;
+    const int32_t *plist = a.large_all ? a.groups.pm_list : a.groups.pl_list;
+    const int n_full = by_size ? __builtin_amdgcn_readfirstlane(fbase[a.G] * NT) : total;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
 
     // token fill: lane l covers row 32 w + l / 4 (+16 for the second
@@ -214,7 +297,15 @@ void k_gemm_bf16(GemmArgs a)
 
     for (int L = first; L < total; L += P) {
         int g, mt, nt;
-        decode_tile(L, tbase, a.G, NT, g, mt, nt);
+        if (L < n_full) {
+            decode_tile(L, by_size ? fbase : tbase, a.G, NT, g, mt, nt);
+        } else {
+            // partial row tiles, largest first; a group's column tiles are consecutive
+            const int j = (L - n_full) / NT;
+            nt = L - n_full - j * NT;
+            g = plist[j];
+            mt = a.groups.rows[g] / kBM;
+        }
         g = __builtin_amdgcn_readfirstlane(g);
         mt = __builtin_amdgcn_readfirstlane(mt);
         nt = __builtin_amdgcn_readfirstlane(nt);
@@ -244,61 +335,18 @@ void k_gemm_bf16(GemmArgs a)
         t.KT = K / kBK;
         t.ncb = min(kBN, N - n0) / 32;
 
-        f32x16 acc[4][2];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int jj = 0; jj < 2; ++jj) acc[i][jj] = (f32x16){};
-
-        fill(t, w, ring[0], 0);
-        fill(t, w, ring[1], 1);
-        fill(t, w, ring[2], 2);
-        // K is a multiple of 128, so KT is a multiple of 4.
-        for (int j = 0; j < t.KT; j += 4) {
-            kstep<0>(t, w, ring, acc, j);
-            kstep<1>(t, w, ring, acc, j + 1);
-            kstep<2>(t, w, ring, acc, j + 2);
-            kstep<3>(t, w, ring, acc, j + 3);
+        // 32-row blocks of this wave's 128-row half that hold rows (uniform per
+        // wave); in band order every tile runs all of them
+        const int nmb = by_size ? __builtin_amdgcn_readfirstlane(
+                                      min(4, max(0, (rows_valid - wm * 128 + 31) >> 5)))
+                                : 4;
+        switch (nmb) {
+        case 0: run_tile<SWIGLU, 0>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+        case 1: run_tile<SWIGLU, 1>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+        case 2: run_tile<SWIGLU, 2>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+        case 3: run_tile<SWIGLU, 3>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+        default: run_tile<SWIGLU, 4>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
         }
-        __syncthreads();   // drain the look-ahead fills before the ring is reused
-
-        // Epilogue.  Accumulator register r of a 32x32 block holds row
-        // 8 (r / 4) + 4 (lane / 32) + r % 4 and column lane % 32.
-        bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
-        // One 32x32 block at a time, so only one block's values are live
-        // outside the accumulators.
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
-                const f32x16 v = acc[mb][nb];
-                const int rbase = wm * 128 + mb * 32 + w.rd_hi * 4;
-                if constexpr (SWIGLU) {
-                    // Packed columns interleave gate and up by 16: in each
-                    // 32-column block, lanes 0-15 hold gate and lanes 16-31 up
-                    // of the same 16 h columns; lane l pairs with lane l ^ 16.
-                    const int f = N / 2;
-                    const bool gl = (lane & 16) == 0;
-                    const int hc = (n0 + wn * 64 + nb * 32) / 2 + (lane & 15);
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const float up = __shfl_xor(v[r], 16);
-                        const int lr = rbase + (r >> 2) * 8 + (r & 3);
-                        if (gl && lr < rows_valid)
-                            C[(int64_t)(row0 + lr) * f + hc] =
-                                f2bf(v[r] / (1.0f + __expf(-v[r])) * up);
-                    }
-                } else {
-                    const int col = n0 + wn * 64 + nb * 32 + (lane & 31);
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int lr = rbase + (r >> 2) * 8 + (r & 3);
-                        if (lr < rows_valid && col < N)
-                            C[(int64_t)(row0 + lr) * N + col] = f2bf(v[r]);
-                    }
-                }
-                __builtin_amdgcn_sched_barrier(0);
-            }
     }
 }
 

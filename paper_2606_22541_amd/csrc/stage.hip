@@ -23,6 +23,7 @@ struct SlotWs {
     int32_t *blk_counts = nullptr, *counts = nullptr, *offsets = nullptr;
     int32_t *g_row0 = nullptr, *g_rows = nullptr, *g_mt_base = nullptr;
     int32_t *g_lt_base = nullptr, *g_st_base = nullptr;
+    int32_t *g_fm_base = nullptr, *g_fl_base = nullptr, *g_pm_list = nullptr, *g_pl_list = nullptr;
     int32_t *slot_of_row = nullptr, *row_of_slot = nullptr;
     void *x_perm = nullptr;
     float *x_perm_s = nullptr;
@@ -95,7 +96,7 @@ Sizes sizes_of(const moe_stage_desc *d)
     const int64_t T1 = T > 0 ? T : 1;
     int64_t b = 0;
     b += align256(s.nb_max * E * 4) + align256(E * 4) + align256((El + 1) * 4);
-    b += 2 * align256(s.G * 4) + 3 * align256((s.G + 1) * 4);
+    b += 2 * align256(s.G * 4) + 7 * align256((s.G + 1) * 4);
     b += align256(cap1 * 4) + align256((s.n_slots_tok > 0 ? s.n_slots_tok : 1) * 4);
     if (fp8) b += align256(cap1 * D) + align256(cap1 * (D / 128) * 4);   // X_perm (fp8 only)
     b += align256(cap1 * F * s.eb) + (fp8 ? align256(cap1 * (F / 128) * 4) : 0);
@@ -352,7 +353,9 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
              alloc(st, &sl.offsets, (El + 1) * 4) &&
              alloc(st, &sl.g_row0, z.G * 4) && alloc(st, &sl.g_rows, z.G * 4) &&
              alloc(st, &sl.g_mt_base, (z.G + 1) * 4) && alloc(st, &sl.g_lt_base, (z.G + 1) * 4) &&
-             alloc(st, &sl.g_st_base, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
+             alloc(st, &sl.g_st_base, (z.G + 1) * 4) && alloc(st, &sl.g_fm_base, (z.G + 1) * 4) &&
+             alloc(st, &sl.g_fl_base, (z.G + 1) * 4) && alloc(st, &sl.g_pm_list, (z.G + 1) * 4) &&
+             alloc(st, &sl.g_pl_list, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
              alloc(st, &sl.row_of_slot, (z.n_slots_tok > 0 ? z.n_slots_tok : 1) * 4) &&
              alloc(st, &sl.h, cap1 * F * z.eb) &&
              alloc(st, &sl.y_perm, cap1 * D * 2);
@@ -443,7 +446,8 @@ static moe_status dispatch_impl(moe_stage *st, int32_t slot, const moe_microbatc
     a.blk_counts = sl.blk_counts;
     a.counts = sl.counts;
     a.offsets = sl.offsets;
-    a.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base};
+    a.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base,
+                          sl.g_fm_base, sl.g_fl_base, sl.g_pm_list, sl.g_pl_list};
     a.slot_of_row = sl.slot_of_row;
     a.row_of_slot = sl.row_of_slot;
     a.err = st->err;
@@ -502,7 +506,8 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     g1.N = 2 * d.d_ff;
     g1.K = d.d_model;
     g1.shared_group = d.has_shared_expert ? d.n_local_experts : -1;
-    g1.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base};
+    g1.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base,
+                          sl.g_fm_base, sl.g_fl_base, sl.g_pm_list, sl.g_pl_list};
     g1.G = (int32_t)st->sz.G;
     g1.layer_id = sl.mb.layer_id;   // weights named on the device (NULL: layer 0)
     g1.layers = st->layers;

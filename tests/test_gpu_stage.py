@@ -233,3 +233,24 @@ def test_max_local_experts_and_group_size_boundaries():
                     device="cuda").to(torch.bfloat16)
     mb = inputs.MicroBatch(x=x, ids=ids, w=rng.random((T, 2)).astype(np.float32))
     _case(cfg, [mb])
+
+
+def test_partial_row_tiles_in_size_order():
+    """The 256-row GEMM runs every group's full row tiles first and then the
+    partial ones by decreasing size.  Group sizes around every tile boundary
+    (0, 1, 31..33, 128/129, 192/193, 255..257, 511..513), two groups with the
+    same partial size (300 and 44 rows), a group with several full tiles
+    (700) and a shared expert over all 4387 tokens; outputs start as NaN, so a
+    tile that no workgroup ran fails the comparison."""
+    sizes = [0, 1, 31, 32, 33, 128, 129, 192, 193, 255, 256, 257, 300, 511, 512, 513, 700, 44]
+    cfg = inputs.MoEConfig("tile_order", d=256, f=128, E=24, e0=0, E_loc=len(sizes), k=1,
+                           lengths=(0,), has_shared=True, seed=12)
+    rng = np.random.default_rng(12)
+    first = np.concatenate([np.full(n, e, np.int32) for e, n in enumerate(sizes)] +
+                           [rng.integers(len(sizes), cfg.E, 300).astype(np.int32)])
+    rng.shuffle(first)
+    T = first.size
+    x = torch.randn((T, cfg.d), generator=torch.Generator("cuda").manual_seed(3),
+                    device="cuda").to(torch.bfloat16)
+    mb = inputs.MicroBatch(x=x, ids=first[:, None].copy(), w=rng.random((T, 1)).astype(np.float32))
+    _case(cfg, [mb])
