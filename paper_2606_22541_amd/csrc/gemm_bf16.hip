@@ -34,14 +34,14 @@
 //    hold rows: each wave takes the instance of its K loop for its number of
 //    such blocks, and a wave whose 128-row half is empty loads no token rows
 //    and runs no MFMAs (it still fills its share of the weight fragments);
-//  * when the last round of the persistent grid would be at most half full,
-//    tiles are numbered full tiles first, then partial tiles in decreasing
-//    order of rows (tables built by the dispatch), so the cheaper partial
-//    tiles form that last round; otherwise the band order below is kept, in
-//    which a partial tile reads its weight panels from L2 beside the full
-//    tiles of its band, and no row blocks are skipped (skipping them there
-//    only shifts power to the other CUs without shortening the longest
-//    list of tiles);
+//  * when the persistent grid runs a single round, or its last round would
+//    be at most half full, tiles are numbered full tiles first, then partial
+//    tiles in decreasing order of rows (tables built by the dispatch), so the
+//    cheaper partial tiles form that last round; otherwise the band order
+//    below is kept, in which a partial tile reads its weight panels from L2
+//    beside the full tiles of its band, and no row blocks are skipped
+//    (skipping them there only shifts power to the other CUs without
+//    shortening the longest list of tiles);
 //  * the tile order is XCD-aware: workgroups are placed round-robin on the 8
 //    XCDs, so consecutive tile numbers are handed to the 32 workgroups of one
 //    XCD, and within a group (full) tiles are rastered in bands of 4 row-tiles,
@@ -274,10 +274,12 @@ void k_gemm_bf16(GemmArgs a)
     const int P = gridDim.x;
     // A last round that fills at most half the grid is worth reordering:
     // full tiles first, then the partial tiles largest first, each running
-    // only its non-empty row blocks.  Otherwise the band order keeps every
-    // partial tile next to the full tiles that share its weight panels in L2.
+    // only its non-empty row blocks.  So is a single round (every workgroup
+    // holds at most one tile, so skipping row blocks only shortens tiles).
+    // Otherwise the band order keeps every partial tile next to the full
+    // tiles that share its weight panels in L2.
     const int tail = total % P;
-    const bool by_size = tail != 0 && 2 * tail <= P;
+    const bool by_size = total <= P || (tail != 0 && 2 * tail <= P);
     const int32_t *fbase = a.large_all ? a.groups.fm_base : a.groups.fl_base;
     const int32_t *plist = a.large_all ? a.groups.pm_list : a.groups.pl_list;
     const int n_full = by_size ? __builtin_amdgcn_readfirstlane(fbase[a.G] * NT) : total;
