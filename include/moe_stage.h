@@ -85,6 +85,8 @@ typedef int32_t moe_status;
 #define MOE_EBUSY          (-6)   /* slot still in flight (non-blocking query) */
 #define MOE_EBADLAYER      (-7)   /* device saw a layer id outside [0, n_layers) */
 #define MOE_ETIMEOUT       (-8)   /* an ingest wait gave up (moe_ingest_wait) */
+#define MOE_EBADCOUNT      (-9)   /* device saw pre-grouped counts that are negative or
+                                     overrun the rows buffer (moe_expert_ffn_grouped) */
 
 enum { MOE_DTYPE_BF16 = 0, MOE_DTYPE_FP8_E4M3_B128 = 1 };
 enum { MOE_COMBINE_OVERWRITE = 0, MOE_COMBINE_ACCUMULATE = 1 };
@@ -145,6 +147,33 @@ typedef struct {
     const int32_t *layer_id;
 } moe_microbatch;
 
+/* A batch of rows that arrives already grouped by local expert: the receive
+ * region of section 3.2.1 in the form Table 2 gives it on the MoE side, with
+ * the senders' per-expert token counts as metadata and one payload row per
+ * (token, local expert) pair.  Device pointers.
+ * rows:       [n_rows_max][d] bf16, or e4m3 in fp8 mode; the rows of local
+ *             expert i are rows [c_0 + ... + c_{i-1}, + c_i), c = counts
+ * row_scales: fp8 mode only, [n_rows_max][d/128] fp32 (moe_quantize_fp8)
+ * counts:     [n_local_experts] int32, read on the device when the work runs
+ *             (the host never learns them); a negative count is taken as 0
+ *             and rows past n_rows_max are dropped (trailing experts lose
+ *             rows), both reported by moe_stage_sync as MOE_EBADCOUNT
+ * y:          [n_rows_max][d] bf16: y_r = W_down (SiLU(W_gate x_r) * (W_up x_r))
+ *             with the weights of the row's expert; rows past the counted
+ *             total are not written.  The routing weights are not applied:
+ *             the weighted sum over a token's k results is formed where the
+ *             results return to (section 3.2.2).
+ * n_rows_max: rows the buffers hold, 0 <= n_rows_max <= capacity_rows
+ * layer_id:   as in moe_microbatch (NULL: layer 0) */
+typedef struct {
+    int32_t        n_rows_max;
+    const void    *rows;
+    const float   *row_scales;
+    const int32_t *counts;
+    void          *y;
+    const int32_t *layer_id;
+} moe_grouped_batch;
+
 /* Device pointers into one slot's workspace (for tests and inspection).
  * Valid after the slot's work has completed; overwritten by its next use. */
 typedef struct {
@@ -187,6 +216,18 @@ MOE_API moe_status moe_dispatch(moe_stage *stage, int32_t slot, const moe_microb
  * down, for every local expert with rows (and the shared expert, if any).
  * The tile schedule is built on the device by moe_dispatch. */
 MOE_API moe_status moe_expert_ffn(moe_stage *stage, int32_t slot, void *stream);
+
+/* Step 2 for pre-grouped rows (moe_grouped_batch): builds the tile tables
+ * on the device from gb->counts, then runs the same grouped GEMMs as
+ * moe_expert_ffn on gb->rows into gb->y, on `slot`'s workspace (H; fp8 also
+ * the transposed row scales).  The stage's shared expert, if any, is not
+ * run (it applies to tokens, not to routed rows).  The slot then holds no
+ * micro-batch: moe_combine on it returns MOE_EINVAL until the next
+ * moe_dispatch.  Host errors (null pointers with n_rows_max > 0, a bad slot,
+ * n_rows_max outside [0, capacity_rows]) return MOE_EINVAL, enqueueing
+ * nothing. */
+MOE_API moe_status moe_expert_ffn_grouped(moe_stage *stage, int32_t slot,
+                                          const moe_grouped_batch *gb, void *stream);
 
 /* Step 3: weighted combine into mb->out (deterministic, no atomics). */
 MOE_API moe_status moe_combine(moe_stage *stage, int32_t slot, void *stream);
@@ -235,8 +276,8 @@ MOE_API moe_status moe_stage_query(moe_stage *stage, int32_t slot, moe_dispatch_
 /* Waits until every slot's enqueued work has completed and returns (then
  * clears) the sticky device errors: MOE_EBADID if a kernel saw an invalid
  * expert id since the last sync, else MOE_EBADLAYER if one saw an invalid
- * layer id, else MOE_ETIMEOUT if an ingest wait gave up, else MOE_OK (or
- * MOE_EHIP). */
+ * layer id, else MOE_EBADCOUNT if one saw invalid pre-grouped counts, else
+ * MOE_ETIMEOUT if an ingest wait gave up, else MOE_OK (or MOE_EHIP). */
 MOE_API moe_status moe_stage_sync(moe_stage *stage);
 
 /* Per-kernel timing with HIP events, for measurement (off by default).

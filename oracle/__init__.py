@@ -9,4 +9,5 @@ from .moe_oracle import (  # noqa: F401
     dispatch, bf16_bits_to_f64, bf16_bits_to_f32, round_f32_to_bf16, e4m3_decode, e4m3_encode,
     quantize_groups, dequantize_groups, dequantize_blocks, silu, swiglu_ffn,
     OracleWeights, stage_inputs_x, run_stage, rel_l2, E4M3_TABLE, E4M3_MAX,
+    grouped_counts, run_grouped,
 )

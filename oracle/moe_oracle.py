@@ -17,9 +17,12 @@ What the stage computes (one device's share of the experts of a MoE layer):
 * The results return as k rows per token and are reduced with the routing
   weights at the receiver (section "Asynchronous Combine", Table 2).
 
-The paper does not write the expert FFN or the combine formula; the readings
-used here (SwiGLU experts, weights applied to expert outputs, ascending-j
-summation) are those of the build's design notes.
+The paper does not write the expert FFN or the combine formula.  This oracle
+takes SwiGLU experts, y = W_down (SiLU(W_gate x) * W_up x), applies the
+routing weights to the expert outputs, and sums a token's results in
+ascending j.  For rows that arrive already grouped by expert (the receive
+region with sender-supplied counts), a negative count is read as 0 and rows
+past the buffer are dropped in expert order.
 
 Arithmetic: every operand is an exact bf16 (or dequantised e4m3) value held in
 fp64, products and sums are fp64, nothing is rounded except where the fp8
@@ -328,6 +331,45 @@ def run_stage(cfg, weights: OracleWeights, x_bits: np.ndarray, ids: np.ndarray,
     res = dict(disp)
     res.update(rows=rows, y=y, tok=tok, out=out, x_codes=x_codes, x_scales=x_scales)
     return res
+
+
+def grouped_counts(counts, n_rows: int) -> np.ndarray:
+    """The per-expert counts a pre-grouped batch is read with: in expert
+    order, a negative count is taken as 0 and an expert keeps only the rows
+    that still fit in the n_rows-row buffer (the stage reports either
+    change as an error; this is the reading the results are defined by)."""
+    kept = []
+    used = 0
+    for c in np.asarray(counts, np.int64).tolist():
+        c = max(c, 0)
+        keep = min(c, max(0, n_rows - used))
+        kept.append(keep)
+        used += keep
+    return np.array(kept, np.int64)
+
+
+def run_grouped(cfg, weights: OracleWeights, rows_x: np.ndarray, counts) -> Dict[str, object]:
+    """Expert FFN of rows that arrive grouped by local expert (the MoE-side
+    receive region of section 3.2.1 and Table 2: the senders supply the
+    per-expert token counts and one payload row per (token, local expert)
+    pair).  Rows [c_0 + ... + c_{i-1}, + c_i) belong to local expert i.
+
+    rows_x: fp64 [n, d], the activations as the FFN sees them (bf16 values,
+    or dequantised e4m3 codes in fp8 mode).  Returns the counts actually
+    used (``grouped_counts``) and ``y`` [sum of them, d]; no routing weight
+    is applied (the weighted sum of a token's results is formed where they
+    return to, section 3.2.2)."""
+    rows_x = np.asarray(rows_x, np.float64)
+    kept = grouped_counts(counts, rows_x.shape[0])
+    quant = cfg.dtype == "fp8"
+    y = np.zeros((int(kept.sum()), cfg.d), np.float64)
+    lo = 0
+    for i, c in enumerate(kept.tolist()):
+        if c:
+            Wg, Wu, Wd = weights.expert(i)
+            y[lo:lo + c], _ = swiglu_ffn(rows_x[lo:lo + c], Wg, Wu, Wd, quantize_h=quant)
+        lo += c
+    return dict(counts=kept, y=y)
 
 
 def rel_l2(a: np.ndarray, ref: np.ndarray) -> float:

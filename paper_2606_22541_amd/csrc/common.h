@@ -32,6 +32,7 @@ constexpr int kBN = 256;
 constexpr int kErrBadId = 1;
 constexpr int kErrBadLayer = 2;
 constexpr int kErrIngestTimeout = 4;
+constexpr int kErrBadCount = 8;       // pre-grouped counts negative or past the rows buffer
 
 // Groups with at most this many rows ("small": a DeepSeek EP32 share at
 // T=4096 has ~128 rows per expert) take one full-height tile in the bf16

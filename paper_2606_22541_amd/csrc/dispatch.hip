@@ -283,6 +283,44 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
     if (b == 0 && wave == 0) build_group_tables(g, tot, E_loc, has_shared, T, lane);
 }
 
+// Tile tables for pre-grouped rows (the receive region of section 3.2.1 in
+// its grouped form: the senders supply the per-expert counts).  One wave:
+// validate the counts in order, then the same table build as the dispatch.
+__global__ __launch_bounds__(64)
+void k_group_tables_from_counts(const int32_t *__restrict__ counts, int32_t E_loc,
+                                int32_t n_rows_max, GroupTable g, int32_t *__restrict__ err)
+{
+    __shared__ int32_t tot[kMaxLocalExperts];
+    const int lane = threadIdx.x;
+    int carry = 0, bad = 0;
+    for (int c0 = 0; c0 < E_loc; c0 += 64) {
+        const int i = c0 + lane;
+        int c = i < E_loc ? counts[i] : 0;
+        bad |= c < 0;
+        c = c < 0 ? 0 : c;
+        int t;
+        const int before = carry + wave_excl_scan(c, lane, t);
+        // rows past n_rows_max are dropped: the group keeps what fits
+        const int keep = min(c, max(0, n_rows_max - before));
+        bad |= keep != c;
+        if (i < E_loc) tot[i] = keep;
+        carry += t;
+    }
+    if (__any(bad) && lane == 0) atomicOr(err, kErrBadCount);
+    __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));   // LDS stores done
+    __builtin_amdgcn_wave_barrier();
+    build_group_tables(g, tot, E_loc, 0, 0, lane);
+}
+
+hipError_t launch_group_tables_from_counts(const int32_t *counts, int32_t E_loc,
+                                           int32_t n_rows_max, GroupTable g, int32_t *err,
+                                           hipStream_t s)
+{
+    hipLaunchKernelGGL(k_group_tables_from_counts, dim3(1), dim3(64), 0, s, counts, E_loc,
+                       n_rows_max, g, err);
+    return hipGetLastError();
+}
+
 hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)
 {
     const int nb = (a.n_slots + kDispatchChunk - 1) / kDispatchChunk;

@@ -25,6 +25,15 @@ struct DispatchArgs {
 // Histogram -> scan (+ GEMM tile table) -> stable scatter.
 hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s);
 
+// Tile tables (GroupTable over the E_loc routed groups, no shared group) for
+// rows that arrive already grouped by local expert: counts[i] rows of expert
+// i, consecutive.  Counts are read on the device; a negative count is taken
+// as 0 and the running total is capped at n_rows_max (later groups lose
+// their rows), both reported through kErrBadCount in *err.
+hipError_t launch_group_tables_from_counts(const int32_t *counts, int32_t E_loc,
+                                           int32_t n_rows_max, GroupTable g, int32_t *err,
+                                           hipStream_t s);
+
 // X_perm[r] = x[slot_of_row[r] / k] for r < offsets[E_loc].  row_bytes is the
 // byte length of one activation row (2d for bf16, d for e4m3); when
 // scales != nullptr the row's fp32 scales (n_scales per row, row-major

@@ -274,6 +274,7 @@ const char *moe_status_string(moe_status s)
     case MOE_EBUSY: return "slot busy";
     case MOE_EBADLAYER: return "layer id outside [0, n_layers) seen on the device (clamped)";
     case MOE_ETIMEOUT: return "an ingest wait gave up before every ready word reached its epoch";
+    case MOE_EBADCOUNT: return "pre-grouped counts negative or past the rows buffer (rows dropped)";
     default: return "unknown status";
     }
 }
@@ -473,6 +474,46 @@ static moe_status dispatch_impl(moe_stage *st, int32_t slot, const moe_microbatc
     return rec ? record(sl, s) : MOE_OK;
 }
 
+// The two grouped GEMMs of one FFN pass on `s`: gate/up with the fused
+// SiLU*up epilogue (fp8: and the quantisation of h), then down.  mt_max bounds
+// the 256-row tiles of all groups together (grid sizes only).
+static moe_status launch_ffn(moe_stage *st, GemmArgs &g1, GemmArgs &g2, int64_t mt_max,
+                             hipStream_t s)
+{
+    const moe_stage_desc &d = st->desc;
+    const bool fp8 = d.dtype == MOE_DTYPE_FP8_E4M3_B128;
+    const int mt = mt_max > 0x7fffffff ? 0x7fffffff : (int)mt_max;
+    const int32_t cap = (int32_t)st->sz.cap, tmax = d.max_tokens;
+    hipError_t e;
+    // bf16: groups of at most kSmallRows rows run in the small-group kernel,
+    // the others in the 256x256-tile kernel (either may find no tiles).
+    const int gmax = (int)st->sz.G;
+    const int cus = stream_cus(st, s);
+    {
+        ProfScope ps(st, 2, s);
+        if (fp8) {
+            e = launch_gemm_fp8(g1, true, mt, gmax, cus, cap, tmax, s);
+        } else {
+            e = launch_gemm_bf16_small(g1, true, gmax, cus, s);
+            if (e == hipSuccess) e = launch_gemm_bf16(g1, true, mt, cus, s);
+        }
+    }
+    if (e == hipSuccess) {
+        ProfScope ps(st, 3, s);
+        if (fp8) {
+            e = launch_gemm_fp8(g2, false, mt, gmax, cus, cap, tmax, s);
+        } else {
+            // the down product (K = f) keeps 256x256 tiles for every group:
+            // at ~130 rows its 28 column tiles per expert already fill the GPU
+            g2.large_all = 1;
+            e = launch_gemm_bf16(g2, false, mt, cus, s);
+        }
+    }
+    if (e == hipErrorNotSupported) return MOE_EUNSUPPORTED;
+    if (e != hipSuccess) return MOE_EHIP;
+    return MOE_OK;
+}
+
 static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
 {
     if (!slot_ok(st, slot)) return MOE_EINVAL;
@@ -533,36 +574,71 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     g2.N = d.d_model;
     g2.K = d.d_ff;
 
-    const int mt = mt_max > 0x7fffffff ? 0x7fffffff : (int)mt_max;
-    const int32_t cap = (int32_t)st->sz.cap, tmax = d.max_tokens;
-    hipError_t e;
-    // bf16: groups of at most kSmallRows rows run in the small-group kernel,
-    // the others in the 256x256-tile kernel (either may find no tiles).
-    const int gmax = (int)st->sz.G;
-    const int cus = stream_cus(st, s);
-    {
-        ProfScope ps(st, 2, s);
-        if (fp8) {
-            e = launch_gemm_fp8(g1, true, mt, gmax, cus, cap, tmax, s);
-        } else {
-            e = launch_gemm_bf16_small(g1, true, gmax, cus, s);
-            if (e == hipSuccess) e = launch_gemm_bf16(g1, true, mt, cus, s);
-        }
-    }
-    if (e == hipSuccess) {
-        ProfScope ps(st, 3, s);
-        if (fp8) {
-            e = launch_gemm_fp8(g2, false, mt, gmax, cus, cap, tmax, s);
-        } else {
-            // the down product (K = f) keeps 256x256 tiles for every group:
-            // at ~130 rows its 28 column tiles per expert already fill the GPU
-            g2.large_all = 1;
-            e = launch_gemm_bf16(g2, false, mt, cus, s);
-        }
-    }
-    if (e == hipErrorNotSupported) return MOE_EUNSUPPORTED;
-    if (e != hipSuccess) return MOE_EHIP;
+    const moe_status r = launch_ffn(st, g1, g2, mt_max, s);
+    if (r != MOE_OK) return r;
     return rec ? record(sl, s) : MOE_OK;
+}
+
+// Pre-grouped rows: the tile tables come from the caller's device counts
+// instead of the dispatch, the gate/up product reads the rows as they are,
+// and the down product writes the caller's y.  No combine follows.
+static moe_status ffn_grouped_impl(moe_stage *st, int32_t slot, const moe_grouped_batch *gb,
+                                   hipStream_t s)
+{
+    if (!slot_ok(st, slot) || !gb) return MOE_EINVAL;
+    const moe_stage_desc &d = st->desc;
+    const bool fp8 = d.dtype == MOE_DTYPE_FP8_E4M3_B128;
+    const int32_t n = gb->n_rows_max;
+    if (n < 0 || n > st->sz.cap) return MOE_EINVAL;
+    if (n > 0 && (!gb->rows || !gb->counts || !gb->y)) return MOE_EINVAL;
+    if (n > 0 && fp8 && !gb->row_scales) return MOE_EINVAL;
+    SlotWs &sl = st->slots[slot];
+    sl.has_mb = false;               // nothing in this slot to combine
+    if (n == 0) return record(sl, s);
+    const GroupTable gt{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base,
+                        sl.g_fm_base, sl.g_fl_base, sl.g_pm_list, sl.g_pl_list};
+    {
+        ProfScope ps(st, 0, s);
+        if (launch_group_tables_from_counts(gb->counts, d.n_local_experts, n, gt, st->err, s) !=
+            hipSuccess)
+            return MOE_EHIP;
+    }
+    if (fp8) {                       // row scales, transposed as the fp8 GEMM reads them
+        ProfScope ps(st, 1, s);
+        if (launch_transpose_scales(gb->row_scales, n, d.d_model / 128, sl.x_perm_s,
+                                    (int32_t)st->sz.cap, s) != hipSuccess)
+            return MOE_EHIP;
+    }
+    GemmArgs g1{};
+    g1.A_routed = gb->rows;
+    g1.As_routed = fp8 ? sl.x_perm_s : nullptr;
+    g1.B = st->w1;
+    g1.Bs = st->s1;
+    g1.C_routed = sl.h;
+    g1.Cs_routed = sl.h_s;
+    g1.N = 2 * d.d_ff;
+    g1.K = d.d_model;
+    g1.shared_group = -1;
+    g1.groups = gt;
+    g1.G = d.n_local_experts;
+    g1.layer_id = gb->layer_id;
+    g1.layers = st->layers;
+    g1.n_layers = d.n_layers;
+    g1.down = 0;
+    g1.err = st->err;
+    GemmArgs g2 = g1;
+    g2.A_routed = sl.h;
+    g2.As_routed = sl.h_s;
+    g2.B = st->w2;
+    g2.Bs = st->s2;
+    g2.C_routed = gb->y;
+    g2.Cs_routed = nullptr;
+    g2.N = d.d_model;
+    g2.K = d.d_ff;
+    g2.down = 1;
+    const moe_status r = launch_ffn(st, g1, g2, ((int64_t)n + kBM - 1) / kBM + d.n_local_experts, s);
+    if (r != MOE_OK) return r;
+    return record(sl, s);
 }
 
 static moe_status combine_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
@@ -597,6 +673,12 @@ moe_status moe_dispatch(moe_stage *st, int32_t slot, const moe_microbatch *mb, v
 moe_status moe_expert_ffn(moe_stage *st, int32_t slot, void *stream)
 {
     return ffn_impl(st, slot, stream, true);
+}
+
+moe_status moe_expert_ffn_grouped(moe_stage *st, int32_t slot, const moe_grouped_batch *gb,
+                                  void *stream)
+{
+    return ffn_grouped_impl(st, slot, gb, (hipStream_t)stream);
 }
 
 moe_status moe_combine(moe_stage *st, int32_t slot, void *stream)
@@ -718,7 +800,10 @@ moe_status moe_stage_sync(moe_stage *st)
         if (hipMemsetAsync(st->err, 0, 4, st->own) != hipSuccess ||
             hipStreamSynchronize(st->own) != hipSuccess)
             return MOE_EHIP;
-        return (err & kErrBadId) ? MOE_EBADID : (err & kErrBadLayer) ? MOE_EBADLAYER : MOE_ETIMEOUT;
+        return (err & kErrBadId)      ? MOE_EBADID
+               : (err & kErrBadLayer) ? MOE_EBADLAYER
+               : (err & kErrBadCount) ? MOE_EBADCOUNT
+                                      : MOE_ETIMEOUT;
     }
     return MOE_OK;
 }

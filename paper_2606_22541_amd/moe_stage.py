@@ -27,6 +27,7 @@ MOE_EUNSUPPORTED = -5
 MOE_EBUSY = -6
 MOE_EBADLAYER = -7
 MOE_ETIMEOUT = -8
+MOE_EBADCOUNT = -9
 MOE_DTYPE_BF16 = 0
 MOE_DTYPE_FP8_E4M3_B128 = 1
 MOE_COMBINE_OVERWRITE = 0
@@ -37,7 +38,7 @@ EXPORTS = (
     "moe_stage_create", "moe_stage_destroy", "moe_dispatch", "moe_expert_ffn", "moe_combine",
     "moe_stage_submit_microbatch", "moe_quantize_fp8", "moe_stage_query", "moe_stage_sync",
     "moe_stage_workspace_bytes", "moe_status_string", "moe_stage_profile",
-    "moe_stage_profile_read", "moe_ingest_wait", "moe_ingest_signal",
+    "moe_stage_profile_read", "moe_ingest_wait", "moe_ingest_signal", "moe_expert_ffn_grouped",
 )
 MOE_PROF_KINDS = 6
 PROF_KIND_NAMES = ("dispatch_index", "gather", "gemm_gate_up_swiglu", "gemm_down", "combine",
@@ -60,6 +61,12 @@ class moe_microbatch(ctypes.Structure):
     _fields_ = [("n_tokens", ctypes.c_int32), ("x", ctypes.c_void_p), ("x_scales", ctypes.c_void_p),
                 ("topk_ids", ctypes.c_void_p), ("topk_w", ctypes.c_void_p), ("out", ctypes.c_void_p),
                 ("combine_mode", ctypes.c_int32), ("layer_id", ctypes.c_void_p)]
+
+
+class moe_grouped_batch(ctypes.Structure):
+    _fields_ = [("n_rows_max", ctypes.c_int32), ("rows", ctypes.c_void_p),
+                ("row_scales", ctypes.c_void_p), ("counts", ctypes.c_void_p),
+                ("y", ctypes.c_void_p), ("layer_id", ctypes.c_void_p)]
 
 
 class moe_dispatch_view(ctypes.Structure):
@@ -109,6 +116,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                         ctypes.POINTER(ctypes.c_int32)]),
         "moe_ingest_wait": (st, [P, P, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint32, P]),
         "moe_ingest_signal": (st, [P, ctypes.c_uint32, P]),
+        "moe_expert_ffn_grouped": (st, [P, ctypes.c_int32, ctypes.POINTER(moe_grouped_batch), P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -189,6 +197,18 @@ def moe_dispatch(stage: int, slot: int, mb: moe_microbatch, stream=None) -> None
 
 def moe_expert_ffn(stage: int, slot: int, stream=None) -> None:
     _check(load_library().moe_expert_ffn(stage, slot, _stream(stream)), "moe_expert_ffn")
+
+
+def make_grouped_batch(n_rows_max, rows, counts, y, row_scales=None,
+                       layer_id=None) -> moe_grouped_batch:
+    """counts: device int32 [n_local_experts]; layer_id as in make_microbatch."""
+    return moe_grouped_batch(int(n_rows_max), _ptr(rows), _ptr(row_scales), _ptr(counts), _ptr(y),
+                             _ptr(layer_id))
+
+
+def moe_expert_ffn_grouped(stage: int, slot: int, gb: moe_grouped_batch, stream=None) -> None:
+    _check(load_library().moe_expert_ffn_grouped(stage, slot, ctypes.byref(gb), _stream(stream)),
+           "moe_expert_ffn_grouped")
 
 
 def moe_combine(stage: int, slot: int, stream=None) -> None:

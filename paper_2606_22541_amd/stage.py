@@ -70,6 +70,13 @@ class ExpertStage:
     def expert_ffn(self, slot, stream=None):
         C.moe_expert_ffn(self.handle, slot, stream)
 
+    def expert_ffn_grouped(self, slot, rows, counts, y, row_scales=None, layer_id=None,
+                           stream=None):
+        """Expert FFN of rows already grouped by local expert (counts: device
+        int32 [E_loc]); y receives one bf16 row per input row."""
+        gb = C.make_grouped_batch(rows.shape[0], rows, counts, y, row_scales, layer_id)
+        C.moe_expert_ffn_grouped(self.handle, slot, gb, stream)
+
     def combine(self, slot, stream=None):
         C.moe_combine(self.handle, slot, stream)
 

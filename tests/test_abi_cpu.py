@@ -43,7 +43,8 @@ def test_library_exports_every_declared_symbol(lib):
 
 def test_status_strings(lib):
     for code in (C.MOE_OK, C.MOE_EINVAL, C.MOE_ENOMEM, C.MOE_EHIP, C.MOE_EBADID,
-                 C.MOE_EUNSUPPORTED, C.MOE_EBUSY, C.MOE_EBADLAYER, C.MOE_ETIMEOUT):
+                 C.MOE_EUNSUPPORTED, C.MOE_EBUSY, C.MOE_EBADLAYER, C.MOE_ETIMEOUT,
+                 C.MOE_EBADCOUNT):
         assert C.moe_status_string(code) not in ("", "unknown status")
     assert C.moe_status_string(12345) == "unknown status"
 
@@ -112,5 +113,7 @@ def test_null_arguments_rejected_without_gpu(lib):
     assert lib.moe_ingest_signal(None, 1, None) == C.MOE_EINVAL
     assert lib.moe_stage_sync(None) == C.MOE_EINVAL
     assert lib.moe_dispatch(None, 0, None, None) == C.MOE_EINVAL
+    gb = C.make_grouped_batch(0, None, None, None)
+    assert lib.moe_expert_ffn_grouped(None, 0, ctypes.byref(gb), None) == C.MOE_EINVAL
     assert lib.moe_stage_create(None, None, None) == C.MOE_EINVAL
     lib.moe_stage_destroy(None)

@@ -216,3 +216,51 @@ def test_fp8_stage_is_bf16_stage_on_dequantised_operands():
             out[t] += w[t, j] * (Wd @ hd)
     np.testing.assert_allclose(res["out"], out, rtol=1e-12, atol=1e-12)
     assert np.array_equal(res["x_codes"], xq)
+
+
+def test_grouped_counts_reading():
+    """Negative counts read as 0; rows past the buffer are dropped in expert order."""
+    assert oracle.grouped_counts([3, -2, 5], 6).tolist() == [3, 0, 3]
+    assert oracle.grouped_counts([0, 0, 0], 4).tolist() == [0, 0, 0]
+    assert oracle.grouped_counts([2, 2], 10).tolist() == [2, 2]
+    assert oracle.grouped_counts([7, 1], 5).tolist() == [5, 0]
+    assert oracle.grouped_counts([], 3).tolist() == []
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_grouped_rows_brute_force(seed):
+    """Each grouped row is its own expert's FFN, checked row by row against
+    the pure-Python SwiGLU; the counts are clamped as read."""
+    rng = np.random.default_rng(300 + seed)
+    d, f, E_loc = 8, 5, 3
+    experts = [tuple(rng.standard_normal(s) * 0.3 for s in ((f, d), (f, d), (d, f)))
+               for _ in range(E_loc)]
+    counts = [int(c) for c in rng.integers(-1, 5, E_loc)]
+    n = int(rng.integers(0, 10))
+    X = rng.standard_normal((n, d))
+    res = oracle.run_grouped(_cfg(d=d, f=f, E_loc=E_loc), _W(experts), X, counts)
+    kept = oracle.grouped_counts(counts, n)
+    assert res["y"].shape == (int(kept.sum()), d)
+    r = 0
+    for e, c in enumerate(kept.tolist()):
+        for _ in range(c):
+            want = bf_swiglu(X[r].tolist(), *[m.tolist() for m in experts[e]])
+            np.testing.assert_allclose(res["y"][r], want, rtol=1e-12, atol=1e-12)
+            r += 1
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_grouped_rows_equal_the_dispatched_rows(dtype):
+    """Rows laid out as the dispatch groups them (x[slot_of_row // k], the
+    local experts' counts) give exactly the stage's per-row results."""
+    rng = np.random.default_rng(41)
+    T, d, f, E, e0, E_loc, k = 24, 128, 128, 8, 2, 4, 3
+    x_bits, ids, w, experts = _rand_problem(rng, T, d, f, E, e0, E_loc, k)
+    cfg = _cfg(d=d, f=f, E=E, e0=e0, E_loc=E_loc, k=k, dtype=dtype)
+    res = oracle.run_stage(cfg, _W(experts), x_bits, ids, w)
+    x_all, _, _ = oracle.stage_inputs_x(x_bits, dtype)
+    rows = x_all[res["slot_of_row"] // k]
+    counts = res["counts"][e0:e0 + E_loc]
+    g = oracle.run_grouped(cfg, _W(experts), rows, counts)
+    assert g["counts"].tolist() == counts.tolist()
+    np.testing.assert_array_equal(g["y"], res["y"])
