@@ -475,6 +475,53 @@ def run_ingest(name="c1", senders=4, rounds=20, warmup=5):
             "host_gating_us_per_round": round((res["host_gated"] - res["device_gated"]) * 1e3, 1)}
 
 
+def run_grouped(name="c1", steps=40, warmup=20, repeats=3):
+    """The pre-grouped input path (moe_expert_ffn_grouped): the micro-batch's
+    local (token, expert) rows laid out grouped by expert before the timed
+    region (torch ops), the per-expert counts in device memory; each step is
+    one moe_expert_ffn_grouped call (tile tables from the counts, then the two
+    grouped GEMMs).  Returns ms per call (median of `repeats` regions)."""
+    import torch
+    from paper_2606_22541_amd import inputs
+    from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
+
+    cfg = inputs.CONFIGS[name]
+    w = inputs.make_weights(cfg, "cuda")
+    mb = inputs.make_microbatches(cfg, "cuda")[0]
+    T = mb.ids.shape[0]
+    ids, _ = to_device_routing(mb.ids, mb.w)
+    flat = ids.reshape(-1).to(torch.int64)
+    local = torch.nonzero((flat >= cfg.e0) & (flat < cfg.e0 + cfg.E_loc)).squeeze(1)
+    key = flat[local] - cfg.e0
+    order = torch.sort(key, stable=True).indices
+    rows = mb.x[local[order] // cfg.k].contiguous()
+    counts = torch.bincount(key, minlength=cfg.E_loc).to(torch.int32)
+    y = torch.empty((rows.shape[0], cfg.d), dtype=torch.bfloat16, device="cuda")
+    stage = ExpertStage(cfg, w, n_slots=1, max_tokens=T)
+    del w
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    times = []
+    for rep in range(repeats + 1):
+        n = warmup if rep == 0 else steps
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(s)
+        for _ in range(n):
+            stage.expert_ffn_grouped(0, rows, counts, y, stream=s)
+        t1.record(s)
+        t1.synchronize()
+        if rep:
+            times.append(t0.elapsed_time(t1) / n)
+    stage.sync()
+    stage.close()
+    times.sort()
+    return {"workload": "%s micro-batch (T=%d) as %d pre-grouped rows with device-side per-expert "
+                        "counts, one moe_expert_ffn_grouped call per step" % (name, T, rows.shape[0]),
+            "ms_per_call": round(times[len(times) // 2], 4),
+            "rows_per_s": round(rows.shape[0] / (times[len(times) // 2] / 1e3), 1)}
+
+
 SWEEP_TOKENS = (512, 1024, 2048, 4096, 8192, 12288, 16384, 24576, 32768)
 
 
@@ -662,6 +709,8 @@ def main():
                     help="also time the dispatch / GEMM / combine three-stream layout (0: skip)")
     ap.add_argument("--ingest", type=int, default=1,
                     help="also time device-gated against host-gated ingest (0: skip)")
+    ap.add_argument("--grouped", type=int, default=1,
+                    help="also time the pre-grouped input path on the primary workload (0: skip)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the latency-vs-tokens sweep of the c1 expert share")
     ap.add_argument("--layers", type=int, default=8,
@@ -734,6 +783,9 @@ def main():
     if args.triple_stream:
         line["%s_triple_stream" % args.workload] = run_triple_stream(args.workload)
         _log("[bench] triple-stream %s done" % args.workload)
+    if args.grouped:
+        line["%s_grouped" % args.workload] = run_grouped(args.workload)
+        _log("[bench] grouped %s done" % args.workload)
     if not args.no_sweep:
         line["token_sweep"] = run_sweep()
         _log("[bench] token sweep done")
