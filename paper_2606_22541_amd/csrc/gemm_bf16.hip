@@ -265,13 +265,17 @@ void k_gemm_bf16(GemmArgs a)
     w.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = w.wave >> 2, wn = w.wave & 3;        // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
-    const void *Bw;
-    const float *Bsw;
-    resolve_weights(a, Bw, Bsw);
     const int NT = (N + kBN - 1) / kBN;
     const int32_t *tbase = a.large_all ? a.groups.mt_base : a.groups.lt_base;
     const int total = __builtin_amdgcn_readfirstlane(tbase[a.G] * NT);
     const int P = gridDim.x;
+    const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
+    // a workgroup without tiles (every one, when no group is this kernel's)
+    // leaves after one load instead of first resolving the weights
+    if (first >= total) return;
+    const void *Bw;
+    const float *Bsw;
+    resolve_weights(a, Bw, Bsw);
     // A last round that fills at most half the grid is worth reordering:
     // full tiles first, then the partial tiles largest first, each running
     // only its non-empty row blocks.  So is a single round (every workgroup
@@ -283,7 +287,6 @@ void k_gemm_bf16(GemmArgs a)
     const int32_t *fbase = a.large_all ? a.groups.fm_base : a.groups.fl_base;
     const int32_t *plist = a.large_all ? a.groups.pm_list : a.groups.pl_list;
     const int n_full = by_size ? __builtin_amdgcn_readfirstlane(fbase[a.G] * NT) : total;
-    const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
 
     // token fill: lane l covers row 32 w + l / 4 (+16 for the second
     // instruction), chunk l % 4; (row / 4) % 4 = (l / 16) % 4 for both

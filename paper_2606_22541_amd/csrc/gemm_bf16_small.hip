@@ -256,13 +256,14 @@ void k_gemm_bf16_small(GemmArgs a)
     w.kh = w.wave >> 1;
     w.ch = w.wave & 1;
     const int N = a.N, K = a.K;
-    const void *Bw;
-    const float *Bsw;
-    resolve_weights(a, Bw, Bsw);
     const int NT = (N + kTNs - 1) / kTNs;
     const int total = __builtin_amdgcn_readfirstlane(a.groups.st_base[a.G] * NT);
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
+    if (first >= total) return;      // no tile: leave before resolving the weights
+    const void *Bw;
+    const float *Bsw;
+    resolve_weights(a, Bw, Bsw);
 
     // fragment-order weights: column block cb of the tile starts at
     // cb * cbstride, sub-step kk of a step at kk KB

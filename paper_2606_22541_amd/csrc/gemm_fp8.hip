@@ -196,14 +196,15 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
     const int lane = w.lane;
     const int wm = w.wave >> 2, wn = w.wave & 3;        // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
-    const void *Bw;
-    const float *Bsw;
-    resolve_weights(a, Bw, Bsw);
     const int NT = (N + kBN - 1) / kBN;
     const int32_t *tbase = kSmall ? a.groups.st_base : a.large_all ? a.groups.mt_base : a.groups.lt_base;
     const int total = __builtin_amdgcn_readfirstlane(tbase[a.G] * NT);
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
+    if (first >= total) return;      // no tile: leave before resolving the weights
+    const void *Bw;
+    const float *Bsw;
+    resolve_weights(a, Bw, Bsw);
 
     // MFMA operand reads: lane l takes row l % 16 of a 16-row block and the
     // 32 bytes [32 (l / 16), 32 (l / 16) + 32) of its 128-byte group (the

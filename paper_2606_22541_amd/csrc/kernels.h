@@ -100,6 +100,8 @@ __device__ __forceinline__ T *uniform_ptr(T *p)
 
 // The weights a GEMM launch uses: a.B / a.Bs, or the ones of the layer named
 // in device memory (read once per workgroup; every wave gets the same value).
+// Workgroup 0 reports an id out of range; it calls this whenever the launch
+// has any tile (a launch without tiles reads no weights and checks nothing).
 __device__ __forceinline__ void resolve_weights(const GemmArgs &a, const void *&B, const float *&Bs)
 {
     B = a.B;
