@@ -16,7 +16,7 @@ typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 // Dispatch: slots handled by one workgroup of the histogram / scatter kernels.
 constexpr int kDispatchThreads = 256;
-constexpr int kDispatchChunk = 2048;            // 8 slots per thread
+constexpr int kDispatchChunk = 1024;            // 4 slots per thread
 constexpr int kMaxExperts = 1024;               // LDS histogram size
 constexpr int kMaxLocalExperts = 256;
 constexpr int kMaxLayers = 1024;
