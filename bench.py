@@ -525,13 +525,31 @@ def run_grouped(name="c1", steps=40, warmup=20, repeats=3):
 SWEEP_TOKENS = (512, 1024, 2048, 4096, 8192, 12288, 16384, 24576, 32768)
 
 
+def sweep_knee(pts, rise=1.5, linear_from=8192):
+    """(knee tokens or None, ms per token of the linear regime or None) of a
+    latency-vs-tokens sweep [{"T", "ms"}, ...] in increasing T."""
+    T = np.array([p["T"] for p in pts], np.float64)
+    ms = np.array([p["ms"] for p in pts], np.float64)
+    knee = None
+    lim = rise * ms[0]
+    for i in range(1, len(pts)):
+        if ms[i] > lim:
+            knee = T[i - 1] + (lim - ms[i - 1]) / (ms[i] - ms[i - 1]) * (T[i] - T[i - 1])
+            break
+    sel = T >= linear_from
+    slope = float(np.polyfit(T[sel], ms[sel], 1)[0]) if np.count_nonzero(sel) >= 2 else None
+    return knee, slope
+
+
 def run_sweep(tokens=SWEEP_TOKENS, steps=10, warmup=5):
     """MoE-stage latency against micro-batch size for the c1 expert share
     (7168 x 2048, 8 of 256 experts local, top-8, uniform routing, bf16): the
     single-GPU analog of the paper's latency-vs-tokens curve under perfect
     balance, which is flat while the weights' HBM stream dominates and turns
-    linear once the grouped GEMM is MFMA-bound.  The knee is where a flat
-    line through the smallest batch meets the line through the two largest."""
+    linear once the grouped GEMM is MFMA-bound.  The flat region ends (the
+    knee) where the latency first exceeds 1.5 times the smallest batch's,
+    interpolated linearly between measured sizes; the marginal cost is the
+    least-squares slope over the sizes from 8192 tokens up."""
     import torch
     from paper_2606_22541_amd import inputs
     from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
@@ -567,16 +585,13 @@ def run_sweep(tokens=SWEEP_TOKENS, steps=10, warmup=5):
                     "rows_per_expert": round(local / cfg.E_loc, 1)})
         del mbs, outs
     stage.close()
-    t0, m0 = pts[0]["T"], pts[0]["ms"]
-    (ta, ma), (tb, mb_) = [(p["T"], p["ms"]) for p in pts[-2:]]
-    slope = (mb_ - ma) / (tb - ta)
-    knee = tb - (mb_ - m0) / slope if slope > 0 else None
+    knee, slope = sweep_knee(pts)
     return {"workload": "c1 expert share at T tokens (d=7168, f=2048, 8 of 256 experts local, "
                         "top-8, uniform, bf16)",
             "points": pts,
             "knee_tokens": round(knee) if knee else None,
             "knee_rows_per_expert": round(knee * cfg.k / cfg.E) if knee else None,
-            "ms_per_1k_tokens_linear": round(slope * 1e3, 4)}
+            "ms_per_1k_tokens_linear": round(slope * 1e3, 4) if slope else None}
 
 
 def run_layers(n_layers, passes=3):
