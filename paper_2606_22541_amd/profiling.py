@@ -149,6 +149,50 @@ def traffic(args):
     print(json.dumps(rec, indent=1, sort_keys=True))
 
 
+# gfx950 MFMA accounting (checked against the kernels' own tile counts):
+# SQ_INSTS_MFMA counts one per MFMA instruction a wave issues, and a
+# v_mfma_f32_32x32x16_bf16 (32768 FLOP) adds 32 to SQ_VALU_MFMA_BUSY_CYCLES;
+# both are summed over the 1024 SIMDs, and GRBM_GUI_ACTIVE over the 8 XCDs.
+SIMDS = 1024
+XCDS = 8
+FLOP_PER_MFMA = 32768
+PEAK_CLOCK_GHZ = 2.4
+
+
+def mfma_util(path: str):
+    """Per GEMM kernel: mean over its dispatches of the duration, the clock
+    (GRBM_GUI_ACTIVE per XCD over the duration), the MFMA instructions and
+    FLOP executed, and the MFMA pipes' busy fraction at that clock and at
+    the nominal 2.4 GHz."""
+    rows = list(csv.DictReader(open(_find_csv(path, "counter_collection.csv"))))
+    per = collections.defaultdict(dict)
+    for r in rows:
+        n = r["Kernel_Name"]
+        if not n.startswith("void moe::k_gemm"):
+            continue
+        d = per[(n.split("(")[0], r["Dispatch_Id"])]
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+        d["ns"] = float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    by_kernel = collections.defaultdict(list)
+    for (name, _), d in per.items():
+        by_kernel[name].append(d)
+    out = {}
+    for name, ds in by_kernel.items():
+        m = {k: sum(d.get(k, 0.0) for d in ds) / len(ds) for k in ds[0]}
+        ns, gui = m["ns"], m["GRBM_GUI_ACTIVE"] / XCDS
+        busy, n_mfma = m["SQ_VALU_MFMA_BUSY_CYCLES"], m["SQ_INSTS_MFMA"]
+        out[name] = {
+            "dispatches": len(ds),
+            "avg_us": ns / 1e3,
+            "clock_ghz": gui / ns if ns else 0.0,
+            "mfma_per_dispatch": n_mfma,
+            "executed_tflops": n_mfma * FLOP_PER_MFMA / ns / 1e3 if ns else 0.0,
+            "mfma_busy_at_clock": busy / (gui * SIMDS) if gui else 0.0,
+            "mfma_busy_at_peak_clock": busy / (ns * PEAK_CLOCK_GHZ * SIMDS) if ns else 0.0,
+        }
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -163,9 +207,13 @@ def main(argv=None):
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--out", required=True)
     t.add_argument("--command", default="")
+    m = sub.add_parser("mfma")
+    m.add_argument("path")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         print(json.dumps(kernel_stats(a.path), indent=1, sort_keys=True))
+    elif a.cmd == "mfma":
+        print(json.dumps(mfma_util(a.path), indent=1, sort_keys=True))
     else:
         traffic(a)
 
