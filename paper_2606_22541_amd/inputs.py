@@ -93,6 +93,11 @@ CONFIGS = {
     # fp8 (e4m3, 128-block scales) variant of c2.
     "c4": MoEConfig("c4", d=7168, f=2048, E=256, e0=0, E_loc=8, k=8, n_micro=4,
                     routing="zipf", dead_local=(6, 7), dtype="fp8"),
+    # fp8 variants of the MFMA-bound shapes, for the fp8 kernel's own rates.
+    "c1p_fp8": MoEConfig("c1p_fp8", d=7168, f=2048, E=256, e0=0, E_loc=8, k=8, lengths=(32768,),
+                         dtype="fp8"),
+    "c3_fp8": MoEConfig("c3_fp8", d=7168, f=2048, E=256, e0=0, E_loc=32, k=8, lengths=(16384,),
+                        has_shared=True, dtype="fp8"),
 }
 
 

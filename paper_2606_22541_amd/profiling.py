@@ -153,10 +153,14 @@ def traffic(args):
 # SQ_INSTS_MFMA counts one per MFMA instruction a wave issues, and a
 # v_mfma_f32_32x32x16_bf16 (32768 FLOP) adds 32 to SQ_VALU_MFMA_BUSY_CYCLES;
 # both are summed over the 1024 SIMDs, and GRBM_GUI_ACTIVE over the 8 XCDs.
+# The fp8 kernel issues v_mfma_scale_f32_16x16x128_f8f6f4 (65536 FLOP).
 SIMDS = 1024
 XCDS = 8
-FLOP_PER_MFMA = 32768
 PEAK_CLOCK_GHZ = 2.4
+
+
+def flop_per_mfma(kernel: str) -> int:
+    return 65536 if "k_gemm_fp8" in kernel else 32768
 
 
 def mfma_util(path: str):
@@ -186,7 +190,8 @@ def mfma_util(path: str):
             "avg_us": ns / 1e3,
             "clock_ghz": gui / ns if ns else 0.0,
             "mfma_per_dispatch": n_mfma,
-            "executed_tflops": n_mfma * FLOP_PER_MFMA / ns / 1e3 if ns else 0.0,
+            "busy_cycles_per_mfma": busy / n_mfma if n_mfma else 0.0,
+            "executed_tflops": n_mfma * flop_per_mfma(name) / ns / 1e3 if ns else 0.0,
             "mfma_busy_at_clock": busy / (gui * SIMDS) if gui else 0.0,
             "mfma_busy_at_peak_clock": busy / (ns * PEAK_CLOCK_GHZ * SIMDS) if ns else 0.0,
         }
