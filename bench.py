@@ -734,9 +734,9 @@ def main():
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU's expert share; runs on %d GPUs are not part of this "
-              "build (the stage shards by expert; see the design notes)." % args.gpus,
-              file=sys.stderr)
+        print("bench.py measures one GPU's expert share and runs on one GPU only (asked for %d); "
+              "across GPUs the stage shards by expert, one process per GPU on its own experts."
+              % args.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"

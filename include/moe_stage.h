@@ -81,7 +81,7 @@ typedef int32_t moe_status;
 #define MOE_ENOMEM         (-2)   /* device allocation failed in create */
 #define MOE_EHIP           (-3)   /* a HIP runtime call failed */
 #define MOE_EBADID         (-4)   /* device saw an expert id outside [-1, n_experts) */
-#define MOE_EUNSUPPORTED   (-5)   /* shape or mode this build does not support */
+#define MOE_EUNSUPPORTED   (-5)   /* shape or mode the library does not support */
 #define MOE_EBUSY          (-6)   /* slot still in flight (non-blocking query) */
 #define MOE_EBADLAYER      (-7)   /* device saw a layer id outside [0, n_layers) */
 #define MOE_ETIMEOUT       (-8)   /* an ingest wait gave up (moe_ingest_wait) */
