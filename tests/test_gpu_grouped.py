@@ -167,3 +167,33 @@ def test_grouped_layer_and_empty_and_host_errors():
         with pytest.raises(C.MoEStageError):
             C.moe_expert_ffn_grouped(st.handle, 5, C.make_grouped_batch(n, rows, dc, y))
     _check_rows(bf16_bits(y), ref["y"], counts, BF16_TOL, "layer 1")
+
+
+def test_counts_across_wave_chunks():
+    """80 local experts: the device reads the counts in chunks of 64 with a
+    running total, and the clamp to the rows buffer falls in the second
+    chunk (expert 70 keeps part of its rows, 71..79 keep none)."""
+    cfg = _cfg("bf16", 54, d=256, f=128, E=96, e0=8, E_loc=80, k=2, lengths=(1000,))
+    wts = inputs.make_weights(cfg, "cuda")
+    ow = oracle.OracleWeights(wts, "bf16")
+    rng = np.random.default_rng(54)
+    counts = rng.integers(0, 30, cfg.E_loc).astype(np.int32)
+    counts[[3, 64, 65]] = [0, 200, 0]                  # a large group opening the second chunk
+    counts[10] = -5
+    n = int(np.maximum(counts, 0)[:70].sum()) + 7      # expert 70 keeps 7 rows
+    kept = oracle.grouped_counts(counts, n)
+    assert kept[70] == min(7, counts[70]) and kept[71:].sum() == 0 and kept[10] == 0
+    rows = torch.from_numpy(rng.standard_normal((n, cfg.d)).astype(np.float32)).to("cuda").to(torch.bfloat16)
+    ref = oracle.run_grouped(cfg, ow, bits_to_f64(bf16_bits(rows)), counts)
+    y = _y_buffer(cfg, n + SPARE)
+    log("grouped: 80 experts, %d rows, clamp inside the second chunk" % n)
+    with ExpertStage(cfg, wts, n_slots=1, max_tokens=cfg.lengths[0]) as st:
+        buf = torch.zeros((n + SPARE, cfg.d), dtype=torch.bfloat16, device="cuda")
+        buf[:n] = rows
+        gb = C.make_grouped_batch(n, buf, torch.from_numpy(counts).to("cuda"), y)
+        C.moe_expert_ffn_grouped(st.handle, 0, gb)
+        with pytest.raises(C.MoEStageError) as e:
+            st.sync()
+        assert e.value.status == C.MOE_EBADCOUNT
+        torch.cuda.synchronize()
+    _check_rows(bf16_bits(y), ref["y"], kept, BF16_TOL, "80 experts")
