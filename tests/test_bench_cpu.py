@@ -1,0 +1,75 @@
+"""Host logic of the measurement, on the CPU: the token-sweep knee, the
+single-GPU guard of bench.py, and the reduction of MFMA counters."""
+import csv
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from paper_2606_22541_amd import profiling  # noqa: E402
+
+
+def _pts(f, Ts=(512, 1024, 2048, 4096, 8192, 16384, 32768)):
+    return [{"T": T, "ms": f(T)} for T in Ts]
+
+
+def test_sweep_knee_flat_then_linear():
+    # flat at 0.2 ms up to 4096 tokens, then 0.05 ms per 1k tokens
+    pts = _pts(lambda T: 0.2 if T <= 4096 else 0.2 + 0.05e-3 * (T - 4096))
+    knee, slope = bench.sweep_knee(pts)
+    # 1.5 x 0.2 = 0.3 ms is reached at 4096 + 0.1 / 0.05e-3 = 6096 tokens
+    assert knee == pytest.approx(6096.0)
+    assert slope == pytest.approx(0.05e-3)
+
+
+def test_sweep_knee_never_rises():
+    knee, slope = bench.sweep_knee(_pts(lambda T: 0.2))
+    assert knee is None
+    assert slope == pytest.approx(0.0, abs=1e-15)
+
+
+def test_bench_refuses_several_gpus():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def _write_counters(path, kernel, ns, values):
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name",
+                                          "Counter_Value", "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        for disp in (1, 2):
+            for name, v in values.items():
+                w.writerow({"Dispatch_Id": disp, "Kernel_Name": kernel + "(moe::GemmArgs)",
+                            "Counter_Name": name, "Counter_Value": v,
+                            "Start_Timestamp": 1000, "End_Timestamp": 1000 + ns})
+
+
+def test_mfma_util_reduction(tmp_path):
+    # 1e6 bf16 MFMAs (32 busy cycles each) in 100 us, GRBM summed over 8 XCDs at 2.0 GHz
+    ns = 100_000
+    n = 1_000_000
+    _write_counters(tmp_path / "run_counter_collection.csv", "void moe::k_gemm_bf16<true>", ns,
+                    {"SQ_INSTS_MFMA": n, "SQ_VALU_MFMA_BUSY_CYCLES": 32 * n,
+                     "GRBM_GUI_ACTIVE": 8 * 2.0 * ns, "SQ_BUSY_CU_CYCLES": 0})
+    r = profiling.mfma_util(str(tmp_path))["void moe::k_gemm_bf16<true>"]
+    assert r["dispatches"] == 2
+    assert r["clock_ghz"] == pytest.approx(2.0)
+    assert r["executed_tflops"] == pytest.approx(n * 32768 / ns / 1e3)
+    # busy cycles over all 1024 SIMDs at 2.0 GHz for 100 us
+    assert r["mfma_busy_at_clock"] == pytest.approx(32 * n / (1024 * 2.0 * ns))
+    assert r["mfma_busy_at_peak_clock"] == pytest.approx(32 * n / (1024 * 2.4 * ns))
+    assert r["busy_cycles_per_mfma"] == pytest.approx(32.0)
+
+
+def test_fp8_mfma_counts_double_flop():
+    assert profiling.flop_per_mfma("void moe::k_gemm_fp8<true, 8>") == 2 * profiling.flop_per_mfma(
+        "void moe::k_gemm_bf16<true>")
