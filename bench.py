@@ -62,13 +62,16 @@ def gemm_accounting(cfg, counts_local, T):
 
 
 def stream_accounting(cfg, counts_local, n_tokens_with_local, T):
-    """Algorithmic bytes of the gather and the combine (overwrite mode)."""
+    """Algorithmic bytes of the dispatch index (ids read; counts, offsets and
+    the two permutation arrays written), the gather and the combine
+    (overwrite mode)."""
     d, k = cfg.d, cfg.k
     n_loc = int(counts_local.sum())
     rb = d * 2
+    index = T * k * 4 + cfg.E * 4 + (cfg.E_loc + 1) * 4 + (n_loc + T * k) * 4
     gather = n_tokens_with_local * rb + n_loc * rb + n_loc * 4
     combine = T * k * 12 + n_loc * rb + T * rb + (T * rb if cfg.has_shared else 0)
-    return dict(gather_bytes=gather, combine_bytes=combine)
+    return dict(index_bytes=index, gather_bytes=gather, combine_bytes=combine)
 
 
 def run_workload(name, steps, warmup, n_buffers=3, repeats=5):
@@ -234,7 +237,12 @@ def stream_rooflines(r):
                                  "peak_tflops": peak_tf}
     if r["kern"].get("quantize_h"):
         out["quantize_h"] = {"avg_ms": round(r["kern"]["quantize_h"], 4)}
-    out["dispatch_index"] = {"avg_ms": round(r["kern"]["dispatch_index"], 4)}
+    t = r["kern"]["dispatch_index"]
+    gbs = a["index_bytes"] / (t / 1e3) / 1e9
+    # a few hundred KB per micro-batch: launch and memory latency, not bandwidth
+    out["dispatch_index"] = {"avg_ms": round(t, 4), "algorithmic_bytes": a["index_bytes"],
+                             "achieved_GBs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                             "bound": "latency"}
     return out
 
 
@@ -246,6 +254,9 @@ WORKLOAD_TEXT = {
           "Zipf(1.2) routing, two dead local experts, bf16",
     "c3": "EP8 share, T=%(T)d, %(El)d of %(E)d experts local plus one shared expert, bf16",
     "c4": "c2 in fp8 (e4m3 with 128-block scales), %(n)d micro-batches %(Ts)s on %(n)d streams",
+    "c1p_fp8": "the c1p share in fp8 (e4m3 with 128-block scales), T=%(T)d",
+    "c3_fp8": "the c3 share in fp8 (e4m3 with 128-block scales), T=%(T)d, %(El)d of %(E)d experts "
+              "local plus one shared expert",
 }
 
 
