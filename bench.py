@@ -69,7 +69,9 @@ def stream_accounting(cfg, counts_local, n_tokens_with_local, T):
     n_loc = int(counts_local.sum())
     rb = d * 2
     index = T * k * 4 + cfg.E * 4 + (cfg.E_loc + 1) * 4 + (n_loc + T * k) * 4
-    gather = n_tokens_with_local * rb + n_loc * rb + n_loc * 4
+    # the gather runs in fp8 mode only: e4m3 codes plus one fp32 scale per 128 channels
+    gb = d + (d // 128) * 4 if cfg.dtype == "fp8" else rb
+    gather = n_tokens_with_local * gb + n_loc * gb + n_loc * 4
     combine = T * k * 12 + n_loc * rb + T * rb + (T * rb if cfg.has_shared else 0)
     return dict(index_bytes=index, gather_bytes=gather, combine_bytes=combine)
 
