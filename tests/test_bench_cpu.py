@@ -73,3 +73,20 @@ def test_mfma_util_reduction(tmp_path):
 def test_fp8_mfma_counts_double_flop():
     assert profiling.flop_per_mfma("void moe::k_gemm_fp8<true, 8>") == 2 * profiling.flop_per_mfma(
         "void moe::k_gemm_bf16<true>")
+
+
+def test_stream_accounting_bytes():
+    """Algorithmic bytes: the dispatch index moves ids and index arrays; the
+    fp8 gather moves e4m3 codes plus one fp32 scale per 128 channels."""
+    import numpy as np
+    from paper_2606_22541_amd import inputs
+    T, U = 4096, 900
+    counts = np.full(8, 132)
+    n_loc = int(counts.sum())
+    c1 = inputs.CONFIGS["c1"]
+    a = bench.stream_accounting(c1, counts, U, T)
+    assert a["index_bytes"] == T * 8 * 4 + 256 * 4 + 9 * 4 + (n_loc + T * 8) * 4
+    assert a["combine_bytes"] == T * 8 * 12 + n_loc * 7168 * 2 + T * 7168 * 2
+    f8 = inputs.CONFIGS["c4"]
+    b = bench.stream_accounting(f8, counts, U, T)
+    assert b["gather_bytes"] == (U + n_loc) * (7168 + 56 * 4) + n_loc * 4
