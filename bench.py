@@ -724,8 +724,8 @@ def cpu_baseline(name="c1", min_seconds=10.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="c1")
     ap.add_argument("--secondary", default="c1p,c3,c2,c4",
                     help="comma-separated further workloads ('' for none)")
