@@ -199,6 +199,15 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
         for (int w = 0; w < kWaves; ++w) wbase[w][i] = 0;
     }
     for (int q = tid; q < n_my; q += kDispatchThreads) cnt_my[q] = 0;
+    // first histogram value of this thread's share of the global counts,
+    // loaded now so that it arrives with the ones below instead of a round
+    // trip later
+    const int n_cnt = n_my * nb_hist;
+    int cnt0 = 0;
+    if (tid < n_cnt) {
+        const int q = tid / nb_hist, bb = tid - q * nb_hist;
+        cnt0 = blk_counts[(int64_t)bb * E + b + q * (int)gridDim.x];
+    }
     __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4) | (0 << 8));   // lgkmcnt(0) only
     __builtin_amdgcn_s_barrier();
 
@@ -230,7 +239,8 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
     for (int j = 0; j < kSteps; ++j)
         if (li[j] >= 0) atomicAdd(&wbase[wave][li[j]], 1);
     // global counts of experts b, b + grid, ...
-    for (int it = tid; it < n_my * nb_hist; it += kDispatchThreads) {
+    if (tid < n_cnt) atomicAdd(&cnt_my[tid / nb_hist], cnt0);
+    for (int it = tid + kDispatchThreads; it < n_cnt; it += kDispatchThreads) {
         const int q = it / nb_hist, bb = it - q * nb_hist;
         atomicAdd(&cnt_my[q], blk_counts[(int64_t)bb * E + b + q * (int)gridDim.x]);
     }
