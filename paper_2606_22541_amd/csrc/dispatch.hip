@@ -162,9 +162,10 @@ __device__ void build_group_tables(const GroupTable &g, const int32_t *tot, int 
 //    the local-expert columns of the histogram rows to get the expert totals
 //    and the counts of the workgroups before it, so no single-workgroup scan
 //    sits between the two kernels.  Workgroup b also writes the global counts
-//    of experts b, b + grid, ...; workgroup 0 writes the offsets and the
-//    grouped-GEMM tile tables.  Within a step, lanes holding the same expert
-//    are ranked by lane order with a ballot.
+//    of experts b, b + grid, ...; workgroup 0 writes the offsets, and the
+//    last workgroup, which owns no slots, the grouped-GEMM tile tables.
+//    Within a step, lanes holding the same expert are ranked by lane order
+//    with a ballot.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kDispatchThreads)
 void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, int32_t E,
@@ -288,9 +289,9 @@ void k_place(const int32_t *__restrict__ ids, int32_t n_slots, int32_t nb_hist, 
             if (pos >= 0) slot_of_row[pos] = (int32_t)sl;
         }
     }
-    // after this wave's own placement, so the other waves and workgroups
-    // place their slots meanwhile
-    if (b == 0 && wave == 0) build_group_tables(g, tot, E_loc, has_shared, T, lane);
+    // the last workgroup owns no slots (the launch adds it for this): its
+    // first wave builds the tables while the others place their slots
+    if (b == (int)gridDim.x - 1 && wave == 0) build_group_tables(g, tot, E_loc, has_shared, T, lane);
 }
 
 // Tile tables for pre-grouped rows (the receive region of section 3.2.1 in
@@ -338,7 +339,8 @@ hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)
         hipLaunchKernelGGL(k_hist, dim3(nb), dim3(kDispatchThreads), 0, s, a.ids, a.n_slots, a.E,
                            a.blk_counts, a.err);
     }
-    hipLaunchKernelGGL(k_place, dim3(nb > 0 ? nb : 1), dim3(kDispatchThreads), 0, s, a.ids,
+    // one workgroup per histogram row, plus one without slots for the tables
+    hipLaunchKernelGGL(k_place, dim3(nb + 1), dim3(kDispatchThreads), 0, s, a.ids,
                        a.n_slots, nb, a.E, a.e0, a.E_loc, a.T, a.has_shared, a.blk_counts,
                        a.counts, a.offsets, a.groups, a.slot_of_row, a.row_of_slot);
     return hipGetLastError();
