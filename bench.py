@@ -147,10 +147,18 @@ def run_workload(name, steps, warmup, n_buffers=3, repeats=5):
     torch.cuda.synchronize()
     ms = region(steps)                                  # timed region: exactly `steps` steps
     spread = sorted([ms / steps] + [region(steps) / steps for _ in range(repeats)])
-    # per-kernel times: the same steps with the library's HIP events
+    # per-kernel times: the same steps with the library's HIP events.  With
+    # several micro-batches the events of overlapping streams would include
+    # each other's kernels, so this pass submits a step's micro-batches one
+    # after another on one stream (kernel rates only; the step time above is
+    # the overlapped one).
     C.moe_stage_profile(stage.handle, True)
     for s in range(steps):
-        step(s)
+        if n_micro == 1:
+            step(s)
+        else:
+            for m in mbs[s % n_sets]:
+                stage.submit(m, main)
     stage.sync()
     torch.cuda.synchronize()
     prof = C.moe_stage_profile_read(stage.handle)
@@ -180,10 +188,12 @@ def run_workload(name, steps, warmup, n_buffers=3, repeats=5):
                         "regions": len(spread)})
 
 
-def measured_traffic(workload, kernel):
+def measured_traffic(workload, kernel, fp8=False):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
     None when it is missing or the kernel's sources changed since."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
+    if fp8 and kernel.startswith("gemm_"):
+        kernel += "_fp8"
     try:
         from paper_2606_22541_amd.profiling import sources_digest
         rec = json.load(open(path))["kernels"]["%s:%s" % (workload, kernel)]
@@ -194,6 +204,49 @@ def measured_traffic(workload, kernel):
         return None
 
 
+STEP_GROUPS = ("dispatch_index", "gather", "gemm_gate_up_swiglu", "gemm_down", "combine")
+
+
+def step_roofline(r):
+    """Roofline of a whole step of a multi-micro-batch workload, whose
+    micro-batches overlap on their own streams: the step's algorithmic FLOPs
+    (both grouped GEMMs) and bytes (every kernel group) over the measured
+    step time.  `traffic` sums the counters' bytes per dispatch of each
+    kernel group times the micro-batches of a step (null unless every group
+    has a current record)."""
+    a = r["acct"]
+    ms = r["ms"] / r["steps"]
+    fp8 = r["cfg"].dtype == "fp8"
+    flop = a["g1_flop"] + a["g2_flop"]
+    byts = a["g1_bytes"] + a["g2_bytes"] + a["index_bytes"] + a["combine_bytes"] + (
+        a["gather_bytes"] if fp8 else 0)
+    peak_tf = PEAK_FP8_TFLOPS if fp8 else PEAK_BF16_TFLOPS
+    traffic = 0
+    for k in STEP_GROUPS:
+        if k == "gather" and not fp8:
+            continue
+        t = measured_traffic(r["cfg"].name, k, fp8)
+        if t is None:
+            traffic = None
+            break
+        traffic += t * r["n_micro"]
+    base = {"kernel": "step: every kernel of the step's %d micro-batches, overlapped on %d streams"
+                      % (r["n_micro"], r["n_micro"]),
+            "traffic": traffic, "algorithmic_flop": flop, "algorithmic_bytes": byts,
+            "avg_ms": round(ms, 4), "tflops": round(flop / (ms / 1e3) / 1e12, 1),
+            "achieved_GBs": round(byts / (ms / 1e3) / 1e9, 1),
+            "floor_ms": round(max(flop / (peak_tf * 1e12), byts / (PEAK_HBM_GBS * 1e9)) * 1e3, 4)}
+    if flop / (peak_tf * 1e12) >= byts / (PEAK_HBM_GBS * 1e9):
+        ach = flop / (ms / 1e3) / 1e12
+        base.update(bound="mfma", achieved=round(ach, 1), peak=peak_tf, unit="TFLOP/s",
+                    frac=round(ach / peak_tf, 4))
+    else:
+        ach = byts / (ms / 1e3) / 1e9
+        base.update(bound="hbm", achieved=round(ach, 1), peak=PEAK_HBM_GBS, unit="GB/s",
+                    frac=round(ach / PEAK_HBM_GBS, 4))
+    return base
+
+
 def roofline_for(r, kernel="gemm_gate_up_swiglu"):
     """Roofline of one launch of `kernel` (per step when the step has one
     micro-batch; summed over the step's micro-batches otherwise)."""
@@ -201,26 +254,28 @@ def roofline_for(r, kernel="gemm_gate_up_swiglu"):
     t = r["kern"][kernel] / 1e3
     flop, byts = (a["g1_flop"], a["g1_bytes"]) if kernel == "gemm_gate_up_swiglu" else (
         a["g2_flop"], a["g2_bytes"])
-    peak_tf = PEAK_FP8_TFLOPS if r["cfg"].dtype == "fp8" else PEAK_BF16_TFLOPS
+    fp8 = r["cfg"].dtype == "fp8"
+    peak_tf = PEAK_FP8_TFLOPS if fp8 else PEAK_BF16_TFLOPS
     t_mfma = flop / (peak_tf * 1e12)
     t_hbm = byts / (PEAK_HBM_GBS * 1e9)
     if t_mfma >= t_hbm:
         ach = flop / t / 1e12
         return {"kernel": kernel, "bound": "mfma", "achieved": round(ach, 1), "peak": peak_tf,
                 "unit": "TFLOP/s", "frac": round(ach / peak_tf, 4),
-                "traffic": measured_traffic(r["cfg"].name, kernel),
+                "traffic": measured_traffic(r["cfg"].name, kernel, fp8),
                 "algorithmic_flop": flop, "algorithmic_bytes": byts, "avg_ms": round(t * 1e3, 4)}
     ach = byts / t / 1e9
     return {"kernel": kernel, "bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
             "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4),
-            "traffic": measured_traffic(r["cfg"].name, kernel),
+            "traffic": measured_traffic(r["cfg"].name, kernel, fp8),
             "algorithmic_flop": flop, "algorithmic_bytes": byts, "avg_ms": round(t * 1e3, 4),
             "tflops": round(flop / t / 1e12, 1)}
 
 
 def stream_rooflines(r):
-    """Per-step time of each kernel group (summed over the step's micro-batches)
-    against its algorithmic bytes or FLOPs."""
+    """Per-step time of each kernel group (summed over the step's micro-batches,
+    which the profiling pass runs one after another on one stream) against its
+    algorithmic bytes or FLOPs."""
     a = r["acct"]
     peak_tf = PEAK_FP8_TFLOPS if r["cfg"].dtype == "fp8" else PEAK_BF16_TFLOPS
     g1k, g2k = "gemm_gate_up_swiglu", "gemm_down"
@@ -688,8 +743,44 @@ def run_layers(n_layers, passes=3):
     }
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_once(name, threads=None):
+    """Seconds for one oracle run of workload `name`'s first micro-batch,
+    optionally with the BLAS pool limited to `threads`."""
+    import oracle
+    import torch
+    from paper_2606_22541_amd import inputs
+    cfg = inputs.CONFIGS[name]
+    dev = "cuda" if torch.cuda.is_available() else "cpu"
+    w = inputs.make_weights(cfg, dev)
+    mb = inputs.make_microbatches(cfg, dev)[0]
+    ow = oracle.OracleWeights(w, cfg.dtype)
+    xb = mb.x.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    del w
+
+    def run():
+        t0 = time.time()
+        oracle.run_stage(cfg, ow, xb, mb.ids, mb.w)
+        return time.time() - t0
+    if threads is None:
+        return run(), mb.ids.shape[0]
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=threads):
+        return run(), mb.ids.shape[0]
+
+
 def cpu_baseline(name="c1", min_seconds=10.0):
-    """The CPU oracle on the full T=4096 micro-batch of the primary workload."""
+    """The CPU oracle on the full T=4096 micro-batch of the primary workload,
+    on all of the host's BLAS threads; also c0 and c1 once on one thread."""
     import oracle
     import torch
     from paper_2606_22541_amd import inputs
@@ -714,11 +805,24 @@ def cpu_baseline(name="c1", min_seconds=10.0):
         if dt >= min_seconds or runs >= 50:
             break
     T = mb.ids.shape[0]
-    return {"value": round(T * runs / dt, 1), "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": "%d x the full %s micro-batch (T=%d, %d local slots), fp64, %.1f s wall" % (
-                runs, name, T,
-                int(np.count_nonzero((mb.ids >= cfg.e0) & (mb.ids < cfg.e0 + cfg.E_loc))), dt)}
+    res = {"value": round(T * runs / dt, 1), "unit": "tokens/s", "cores": int(threads),
+           "kind": "oracle",
+           "sample": "%d x the full %s micro-batch (T=%d, %d local slots), fp64, %.1f s wall" % (
+               runs, name, T,
+               int(np.count_nonzero((mb.ids >= cfg.e0) & (mb.ids < cfg.e0 + cfg.E_loc))), dt),
+           "cpu_model": cpu_model(), "nproc": os.cpu_count(),
+           "affinity_cpus": len(os.sched_getaffinity(0))}
+    del ow, mb
+    single = {}
+    for wl in ("c0", name):
+        try:
+            sec, Tw = _oracle_once(wl, threads=1)
+            single[wl] = {"tokens_per_s": round(Tw / sec, 1), "seconds": round(sec, 3),
+                          "tokens": Tw}
+        except Exception as e:          # threadpoolctl missing: report why
+            single[wl] = {"error": repr(e)}
+    res["single_thread"] = single
+    return res
 
 
 def main():
@@ -801,9 +905,15 @@ def main():
             "tokens_per_s": round(sec["T"] * sec["steps"] / (sec["ms"] / 1e3), 1),
             "ms_per_step": round(sec["ms"] / sec["steps"], 4),
             "spread_ms_per_step": sec["spread"],
-            "roofline": roofline_for(sec),
-            "kernels": stream_rooflines(sec),
         }
+        if sec["n_micro"] > 1:
+            # overlapping streams: the roofline is the step's; kernel rates
+            # come from a pass with the micro-batches one after another
+            line[name]["roofline"] = step_roofline(sec)
+            line[name]["kernels_serialized"] = stream_rooflines(sec)
+        else:
+            line[name]["roofline"] = roofline_for(sec)
+            line[name]["kernels"] = stream_rooflines(sec)
         _log("[bench] %s done" % name)
     if args.pipelined_streams > 1:
         line["%s_pipelined" % args.workload] = run_pipelined(args.workload, args.pipelined_streams)

@@ -52,10 +52,10 @@
  *                    (MOE_COMBINE_ACCUMULATE), plus the shared expert's
  *                    output when the stage has one.
  * Intermediate rows (H, Y_perm) are stored in bf16 (fp8 mode: X_perm and H
- * as e4m3 with per-128-channel fp32 scales, h being rounded to bf16 before it
- * is quantised).  In bf16 mode X_perm is never materialised: the gate/up
- * grouped GEMM loads row r straight from x[slot_of_row[r] / k] (the row
- * gather is fused into its token-row loads).  The combine accumulates in
+ * as e4m3 with per-128-channel fp32 scales; h is quantised from its fp32
+ * value by the rule of moe_quantize_fp8).  In bf16 mode X_perm is never
+ * materialised: the gate/up grouped GEMM loads row r straight from
+ * x[slot_of_row[r] / k] (the row gather is fused into its token-row loads).  The combine accumulates in
  * fp32 and rounds once to bf16.  Tokens with no local slot are written as
  * +0.0 (overwrite) or left untouched (accumulate).  The combine uses no
  * atomics, so results are bit-identical from run to run and independent of
@@ -82,7 +82,7 @@ typedef int32_t moe_status;
 #define MOE_EHIP           (-3)   /* a HIP runtime call failed */
 #define MOE_EBADID         (-4)   /* device saw an expert id outside [-1, n_experts) */
 #define MOE_EUNSUPPORTED   (-5)   /* shape or mode the library does not support */
-#define MOE_EBUSY          (-6)   /* slot still in flight (non-blocking query) */
+#define MOE_EBUSY          (-6)   /* slot still in flight (moe_stage_poll) */
 #define MOE_EBADLAYER      (-7)   /* device saw a layer id outside [0, n_layers) */
 #define MOE_ETIMEOUT       (-8)   /* an ingest wait gave up (moe_ingest_wait) */
 #define MOE_EBADCOUNT      (-9)   /* device saw pre-grouped counts that are negative or
@@ -193,7 +193,9 @@ typedef struct {
     int32_t  n_tokens;        /* T of the micro-batch last dispatched here */
 } moe_dispatch_view;
 
-/* Validates `desc`, copies the weights of its n_layers layers
+/* Validates `desc` (MOE_EUNSUPPORTED when d_model or d_ff is not a multiple
+ * of 128, MOE_EINVAL for any other bad field), copies the weights of its
+ * n_layers layers
  * (weights[0 .. n_layers-1]) into stage-owned HBM, packed for the grouped
  * GEMM, builds the on-device table of the layers' weight addresses, and
  * allocates all workspace for n_slots micro-batches of up to max_tokens
@@ -269,6 +271,14 @@ MOE_API moe_status moe_ingest_wait(moe_stage *stage, const uint32_t *ready, int3
  * its rows are written, or the MoE side acknowledging a consumed round so the
  * senders may overwrite the buffers (backpressure). */
 MOE_API moe_status moe_ingest_signal(uint32_t *word, uint32_t epoch, void *stream);
+
+/* Non-blocking test of one slot (section 3.2.1: a receiver looks at a
+ * region without waiting for it): MOE_OK when the work last enqueued on
+ * `slot` has completed (or the slot was never used), MOE_EBUSY while it is
+ * still in flight, MOE_EINVAL for a bad slot.  Never waits and never
+ * enqueues anything; the host may use it to pick a free slot or to decide
+ * whether the next submit would make its stream wait. */
+MOE_API moe_status moe_stage_poll(moe_stage *stage, int32_t slot);
 
 /* Fills `out` with the device pointers of `slot`'s workspace. */
 MOE_API moe_status moe_stage_query(moe_stage *stage, int32_t slot, moe_dispatch_view *out);

@@ -26,9 +26,11 @@ past the buffer are dropped in expert order.
 
 Arithmetic: every operand is an exact bf16 (or dequantised e4m3) value held in
 fp64, products and sums are fp64, nothing is rounded except where the fp8
-variant quantises the intermediate activation h (the same rule the stage
-uses).  The counting sort is plain C (``dispatch.c``); the dense products use
-numpy's float64 matmul as a library primitive.
+variant quantises the intermediate activation h: per row and 128 channels,
+scale = amax / 448 and code = e4m3(h / scale), both in fp32, the rule the
+activations are quantised by.  The counting sort is plain C
+(``dispatch.c``); the dense products use numpy's float64 matmul as a library
+primitive.
 """
 from __future__ import annotations
 
@@ -194,16 +196,17 @@ def swiglu_ffn(X: np.ndarray, Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray,
     """y = W_down (SiLU(W_gate x) * W_up x) for each row x of X, in fp64.
 
     X [n, d]; Wg, Wu [f, d]; Wd [d, f].  With ``quantize_h`` (the fp8 variant)
-    the intermediate h is rounded to fp32, then to bf16, and quantised per
-    128 channels to e4m3 before the down projection: the stage quantises its
-    bf16 copy of h, so the codes are decided from the same precision.
+    the intermediate h is quantised per row and 128 channels to e4m3 before
+    the down projection, by the same rule as the activations: the scale and
+    the quotient are fp32 quantities, so h enters the quantiser as its fp32
+    value (one rounding of the fp64 h) and nothing else is rounded.
     Returns (y [n, d], h [n, f]).
     """
     g = X @ Wg.T
     u = X @ Wu.T
     h = silu(g) * u
     if quantize_h:
-        codes, scales = quantize_groups(round_f32_to_bf16(h.astype(np.float32)))
+        codes, scales = quantize_groups(h.astype(np.float32))
         h = dequantize_groups(codes, scales)
     y = h @ Wd.T
     return y, h

@@ -183,6 +183,10 @@ __device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLd
         small_step<NMB, 0>(t, l, w, acc, k, breg);
         small_step<NMB, 1>(t, l, w, acc, k + 1, breg);
     }
+    // The look-ahead fills of steps KT..KT+2 (clamped re-reads of the last
+    // step) may still be landing in ring buffers 0-2, which the K-half
+    // partials overwrite next: wait for every load of this wave, then sync.
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0)
     __syncthreads();   // all ring reads done: the ring now holds the K-half partials
 
     // wave (1, ch) hands its partial sums to wave (0, ch), lane-contiguous

@@ -34,9 +34,9 @@
 //    only moves along K (clamped to the last group) and between weight
 //    column blocks that exist;
 //  * SwiGLU mode: the up waves hand their accumulators to the gate waves
-//    through LDS, the gate waves form h = SiLU(gate) * up, round it to bf16
-//    and quantise each row's 128 channels to e4m3 with one fp32 scale (the
-//    same arithmetic as the activation quantiser), and the tile's 256 rows
+//    through LDS, the gate waves form h = SiLU(gate) * up in fp32 and
+//    quantise each row's 128 channels to e4m3 with one fp32 scale (the same
+//    arithmetic as the activation quantiser), and the tile's 256 rows
 //    of 128 codes are written out through LDS as 16-byte stores.  The down
 //    product writes bf16.
 #include "kernels.h"
@@ -310,7 +310,7 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
             }
             __syncthreads();
             if (!(wn & 1)) {
-                // h in bf16 (kept in acc), then this wave's maximum of |h| over
+                // h in fp32 (kept in acc), then this wave's maximum of |h| over
                 // its 64 channels of each row, stored for the partner wave
                 float *mx = q ? lds_s1 : lds_s0;
 #pragma unroll
@@ -322,7 +322,7 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
                             const float gt = acc[rb][cb][i];
-                            const float hv = bf2f(f2bf(gt / (1.0f + __expf(-gt)) * up[i]));
+                            const float hv = gt / (1.0f + __expf(-gt)) * up[i];
                             acc[rb][cb][i] = hv;
                             am[i] = fmaxf(am[i], fabsf(hv));
                         }

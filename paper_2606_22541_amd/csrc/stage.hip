@@ -47,6 +47,19 @@ struct Sizes {
     int64_t per_slot;                       // bytes
 };
 
+bool desc_ok(const moe_stage_desc *d);
+
+// MOE_OK, MOE_EINVAL for a malformed descriptor, or MOE_EUNSUPPORTED for a
+// well-formed shape the kernels do not take: d or f not a multiple of 128
+// (one K step of every GEMM is 128 bytes of fp8 or a multiple of 64 bf16).
+moe_status desc_check(const moe_stage_desc *d)
+{
+    if (!d) return MOE_EINVAL;
+    if (d->d_model <= 0 || d->d_ff <= 0) return MOE_EINVAL;
+    if (d->d_model % 128 || d->d_ff % 128) return MOE_EUNSUPPORTED;
+    return desc_ok(d) ? MOE_OK : MOE_EINVAL;
+}
+
 bool desc_ok(const moe_stage_desc *d)
 {
     if (!d) return false;
@@ -282,7 +295,8 @@ const char *moe_status_string(moe_status s)
 moe_status moe_stage_workspace_bytes(const moe_stage_desc *desc, int64_t *bytes)
 {
     if (!bytes) return MOE_EINVAL;
-    if (!desc_ok(desc)) return MOE_EINVAL;
+    const moe_status dc = desc_check(desc);
+    if (dc != MOE_OK) return dc;
     Sizes s = sizes_of(desc);
     *bytes = s.w1 + s.w2 + s.s1 + s.s2 + 256 + align256(desc->n_layers * (int64_t)sizeof(LayerWeights)) +
              s.per_slot * desc->n_slots;
@@ -293,7 +307,9 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
 {
     if (!out) return MOE_EINVAL;
     *out = nullptr;
-    if (!desc_ok(desc) || !w) return MOE_EINVAL;
+    const moe_status dc = desc_check(desc);
+    if (dc != MOE_OK) return dc;
+    if (!w) return MOE_EINVAL;
     const bool fp8 = desc->dtype == MOE_DTYPE_FP8_E4M3_B128;
     for (int l = 0; l < desc->n_layers; ++l) {
         const moe_weights &wl = w[l];
@@ -718,6 +734,17 @@ moe_status moe_quantize_fp8(const void *x_bf16, int32_t T, int32_t d, void *x_q,
         hipSuccess)
         return MOE_EHIP;
     return MOE_OK;
+}
+
+moe_status moe_stage_poll(moe_stage *st, int32_t slot)
+{
+    if (!slot_ok(st, slot)) return MOE_EINVAL;
+    SlotWs &sl = st->slots[slot];
+    if (!sl.ev_recorded) return MOE_OK;
+    const hipError_t e = hipEventQuery(sl.ev);
+    if (e == hipSuccess) return MOE_OK;
+    if (e == hipErrorNotReady) return MOE_EBUSY;
+    return MOE_EHIP;
 }
 
 moe_status moe_stage_query(moe_stage *st, int32_t slot, moe_dispatch_view *v)

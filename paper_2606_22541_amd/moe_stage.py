@@ -39,6 +39,7 @@ EXPORTS = (
     "moe_stage_submit_microbatch", "moe_quantize_fp8", "moe_stage_query", "moe_stage_sync",
     "moe_stage_workspace_bytes", "moe_status_string", "moe_stage_profile",
     "moe_stage_profile_read", "moe_ingest_wait", "moe_ingest_signal", "moe_expert_ffn_grouped",
+    "moe_stage_poll",
 )
 MOE_PROF_KINDS = 6
 PROF_KIND_NAMES = ("dispatch_index", "gather", "gemm_gate_up_swiglu", "gemm_down", "combine",
@@ -108,6 +109,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "moe_quantize_fp8": (st, [P, ctypes.c_int32, ctypes.c_int32, P, P, P]),
         "moe_stage_query": (st, [P, ctypes.c_int32, ctypes.POINTER(moe_dispatch_view)]),
         "moe_stage_sync": (st, [P]),
+        "moe_stage_poll": (st, [P, ctypes.c_int32]),
         "moe_stage_workspace_bytes": (st, [ctypes.POINTER(moe_stage_desc),
                                            ctypes.POINTER(ctypes.c_int64)]),
         "moe_status_string": (ctypes.c_char_p, [st]),
@@ -232,6 +234,15 @@ def moe_stage_query(stage: int, slot: int) -> moe_dispatch_view:
     v = moe_dispatch_view()
     _check(load_library().moe_stage_query(stage, slot, ctypes.byref(v)), "moe_stage_query")
     return v
+
+
+def moe_stage_poll(stage: int, slot: int) -> int:
+    """MOE_OK when the slot's last work has completed, MOE_EBUSY while it is
+    in flight (raises on any other status)."""
+    r = load_library().moe_stage_poll(stage, slot)
+    if r not in (MOE_OK, MOE_EBUSY):
+        raise MoEStageError(r, "moe_stage_poll")
+    return r
 
 
 def moe_stage_sync(stage: int) -> None:

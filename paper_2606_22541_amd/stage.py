@@ -47,6 +47,7 @@ class ExpertStage:
         self.max_tokens = cfg.max_tokens if max_tokens is None else max_tokens
         layers = list(weights) if isinstance(weights, (list, tuple)) else [weights]
         self.n_layers = len(layers)
+        self.n_slots = n_slots
         self.desc = C.make_desc(cfg.d, cfg.f, cfg.E, cfg.e0, cfg.E_loc, cfg.k, self.max_tokens,
                                 n_slots, C.MOE_DTYPE_FP8_E4M3_B128 if self.fp8 else C.MOE_DTYPE_BF16,
                                 int(cfg.has_shared), self.n_layers)

@@ -1,5 +1,7 @@
 """Helpers shared by the GPU parity tests: run the HIP stage and the oracle on
 the same seeded inputs and compare them."""
+import ctypes
+
 import numpy as np
 import torch
 
@@ -69,8 +71,36 @@ def check_dispatch(view, ref, cfg, mb=None):
         assert np.array_equal(view["x_perm_scales"], ref["x_scales"][tok]), "fp8 X_perm scales differ"
 
 
+def row_rel_l2(got, want):
+    """Per-row ||got - want|| / ||want|| (fp64); rows whose reference is zero
+    give 0 when the row is zero too, else inf."""
+    num = np.sqrt(np.sum((got - want) ** 2, axis=1))
+    den = np.sqrt(np.sum(want ** 2, axis=1))
+    out = np.zeros(num.shape)
+    nz = den > 0
+    out[nz] = num[nz] / den[nz]
+    out[~nz & (num > 0)] = np.inf
+    return out
+
+
+def _check_rows(got, want, tol, label, what):
+    """Every row within `tol` (relative L2 of the row); logs the worst row."""
+    if got.shape[0] == 0:
+        return 0.0
+    errs = row_rel_l2(got, want)
+    worst = int(np.argmax(errs))
+    log("  %s: %d rows, worst row %d rel-L2 %.3e (whole %.3e)" % (
+        label, got.shape[0], worst, errs[worst], oracle.rel_l2(got, want)))
+    bad = np.nonzero(errs > tol)[0]
+    assert bad.size == 0, "%s: %d rows above %.1e, e.g. row %d at %.3e %s" % (
+        label, bad.size, tol, bad[0], errs[bad[0]], what)
+    return float(errs[worst])
+
+
 def check_outputs(out_bits, ref, tol, what=""):
-    """Compares the GPU output rows of the oracle's tokens."""
+    """Compares the GPU output rows of the oracle's tokens: the whole output
+    and every token row within `tol`, no NaN or Inf, and tokens without a
+    local slot (overwrite mode) exactly +0.0."""
     tok = ref["tok"]
     got = bits_to_f64(out_bits[tok])
     want = ref["out"]
@@ -80,6 +110,7 @@ def check_outputs(out_bits, ref, tol, what=""):
         assert np.all(out_bits[tok][zero] == 0), "tokens without local slots must be +0.0 " + what
     err = oracle.rel_l2(got, want)
     assert err <= tol, "rel-L2 %.3e > %.1e %s" % (err, tol, what)
+    _check_rows(got, want, tol, "out rows", what)
     return err
 
 
@@ -89,7 +120,19 @@ def check_expert_rows(view, ref, cfg, tol, what=""):
 
 
 def _check_expert_rows(view, ref, cfg, tol, what=""):
-    """Per-expert rel-L2 of the GPU's Y_perm rows against the oracle's y."""
+    """Per-expert rel-L2 of the GPU's Y_perm rows against the oracle's y, and
+    every row on its own; every row of Y_perm (and H) below the local row
+    count must be finite, which catches a tile that no workgroup wrote when
+    the workspace was poisoned with NaN before the run."""
+    n = int(ref["offsets"][-1])
+    if "y_perm" in view and n:
+        assert np.all(np.isfinite(bits_to_f64(view["y_perm"][:n]))), "non-finite Y_perm row " + what
+    if "h" in view and n:
+        h = view["h"][:n]
+        if h.dtype == np.uint16:
+            assert np.all(np.isfinite(bits_to_f64(h))), "non-finite H row " + what
+        else:     # e4m3 codes: 0x7f / 0xff are NaN
+            assert not np.any((h & 0x7F) == 0x7F), "NaN code in H " + what
     rows = ref["rows"]
     if rows.size == 0:
         return {}
@@ -102,12 +145,72 @@ def _check_expert_rows(view, ref, cfg, tol, what=""):
             e = oracle.rel_l2(got[m], ref["y"][m])
             errs[i] = e
             assert e <= tol, "expert %d rel-L2 %.3e > %.1e %s" % (i, e, tol, what)
+    _check_rows(got, ref["y"], tol, "Y_perm rows", what)
     return errs
 
 
-def sample_tokens(T, n, seed=0):
-    if T <= n:
-        return np.arange(T)
-    rng = np.random.default_rng(seed)
-    s = set(rng.choice(T, size=n - 2, replace=False).tolist()) | {0, T - 1}
-    return np.array(sorted(s))
+def poison_workspace(stage):
+    """Fills every slot's H, Y_perm (and shared-expert) rows with NaN bytes
+    (0xff: NaN in bf16 and in e4m3), so that a row the GPU never writes
+    fails the finiteness checks."""
+    hip = _hip()
+    cfg = stage.cfg
+    eb = 1 if stage.fp8 else 2
+    for sl in range(stage.n_slots):
+        v = C.moe_stage_query(stage.handle, sl)
+        cap = v.capacity_rows
+        for ptr, nbytes in ((v.h, cap * cfg.f * eb), (v.y_perm, cap * cfg.d * 2)):
+            if ptr and nbytes:
+                assert hip.hipMemset(ctypes.c_void_p(ptr), 0xFF, ctypes.c_size_t(nbytes)) == 0
+    assert hip.hipDeviceSynchronize() == 0
+
+
+_hip_handle = None
+
+
+def _hip():
+    global _hip_handle
+    if _hip_handle is None:
+        _hip_handle = ctypes.CDLL("libamdhip64.so")
+        _hip_handle.hipMemset.restype = ctypes.c_int
+        _hip_handle.hipMemset.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t]
+        _hip_handle.hipDeviceSynchronize.restype = ctypes.c_int
+    return _hip_handle
+
+
+class CachedWeights:
+    """OracleWeights whose decoded experts are kept after first use (fp8
+    decoding of a DeepSeek-sized expert takes about a second; micro-batches
+    of one stage reuse them)."""
+
+    def __init__(self, ow):
+        self.ow = ow
+        self.dtype = ow.dtype
+        self._cache = {}
+
+    def expert(self, i):
+        if i not in self._cache:
+            self._cache[i] = self.ow.expert(i)
+        return self._cache[i]
+
+    def shared(self):
+        if "sh" not in self._cache:
+            self._cache["sh"] = self.ow.shared()
+        return self._cache["sh"]
+
+
+def band_order_tiles(rows_per_group, N, small_rows=192, tile=256):
+    """Tiles of the 256-row GEMM over groups of more than `small_rows` rows
+    with N output columns, the persistent grid it runs on (one workgroup per
+    CU, a multiple of 8), and whether it takes the size order: a single round,
+    or a last round at most half full.  Mirrors the launch's documented rule
+    so a test can assert which order a case exercises."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    nt = -(-N // tile)
+    total = sum(-(-int(r) // tile) for r in rows_per_group if r > small_rows) * nt
+    P = min(cus, total)
+    if P >= 8:
+        P &= ~7
+    tail = total % P if P else 0
+    by_size = total <= P or (tail != 0 and 2 * tail <= P)
+    return total, P, by_size

@@ -91,8 +91,20 @@ def test_workspace_bytes_scale_with_layers(lib):
         assert w <= per_layer < w + 2**20
 
 
+@pytest.mark.parametrize("bad", [dict(d_model=200), dict(d_ff=100), dict(d_model=7168 + 64)])
+def test_unsupported_shape_rejected(lib, bad):
+    """d or f not a multiple of 128 is a well-formed shape the kernels do not
+    take: MOE_EUNSUPPORTED, not MOE_EINVAL."""
+    args = dict(d_model=256, d_ff=128, n_experts=8, first_local_expert=0, n_local_experts=4,
+                top_k=2, max_tokens=64, n_slots=1, dtype=0, has_shared_expert=0, n_layers=1)
+    args.update(bad)
+    with pytest.raises(C.MoEStageError) as e:
+        C.moe_stage_workspace_bytes(C.moe_stage_desc(**args))
+    assert e.value.status == C.MOE_EUNSUPPORTED
+
+
 @pytest.mark.parametrize("bad", [
-    dict(d_model=200), dict(d_ff=100), dict(n_experts=0), dict(n_experts=2000),
+    dict(d_model=0), dict(d_ff=-128), dict(n_experts=0), dict(n_experts=2000),
     dict(n_local_experts=0), dict(first_local_expert=250), dict(top_k=0), dict(top_k=33),
     dict(max_tokens=-1), dict(n_slots=0), dict(dtype=7), dict(has_shared_expert=2),
     dict(n_layers=0), dict(n_layers=-3), dict(n_layers=1025),
@@ -116,4 +128,5 @@ def test_null_arguments_rejected_without_gpu(lib):
     gb = C.make_grouped_batch(0, None, None, None)
     assert lib.moe_expert_ffn_grouped(None, 0, ctypes.byref(gb), None) == C.MOE_EINVAL
     assert lib.moe_stage_create(None, None, None) == C.MOE_EINVAL
+    assert lib.moe_stage_poll(None, 0) == C.MOE_EINVAL
     lib.moe_stage_destroy(None)

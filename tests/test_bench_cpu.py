@@ -90,3 +90,23 @@ def test_stream_accounting_bytes():
     f8 = inputs.CONFIGS["c4"]
     b = bench.stream_accounting(f8, counts, U, T)
     assert b["gather_bytes"] == (U + n_loc) * (7168 + 56 * 4) + n_loc * 4
+
+
+def test_step_roofline_of_overlapped_micro_batches():
+    """Multi-stream workloads report the whole step: both GEMMs' FLOPs and
+    every kernel group's bytes over the measured step time."""
+    from paper_2606_22541_amd import inputs
+    acct = dict(g1_flop=4e12, g2_flop=2e12, g1_bytes=1e9, g2_bytes=0.5e9, index_bytes=1e6,
+                combine_bytes=2e8, gather_bytes=1e8)
+    r = dict(cfg=inputs.CONFIGS["c2"], acct=acct, ms=40.0, steps=20, n_micro=4)
+    ro = bench.step_roofline(r)
+    # 6 TFLOP / 2 ms = 3000 TFLOP/s against bf16; MFMA time 2.4 ms > HBM time 0.21 ms
+    assert ro["bound"] == "mfma" and ro["peak"] == bench.PEAK_BF16_TFLOPS
+    assert ro["achieved"] == pytest.approx(3000.0)
+    assert ro["frac"] == pytest.approx(1.2)
+    assert ro["algorithmic_bytes"] == 1e9 + 0.5e9 + 1e6 + 2e8        # bf16: no gather kernel
+    assert ro["floor_ms"] == pytest.approx(6e12 / 2.5e15 * 1e3)
+    r8 = dict(r, cfg=inputs.CONFIGS["c4"])
+    ro8 = bench.step_roofline(r8)
+    assert ro8["peak"] == bench.PEAK_FP8_TFLOPS
+    assert ro8["algorithmic_bytes"] == 1e9 + 0.5e9 + 1e6 + 2e8 + 1e8  # fp8 gathers X_perm

@@ -12,8 +12,8 @@ import oracle
 from paper_2606_22541_amd import inputs
 from paper_2606_22541_amd.stage import ExpertStage, bf16_bits, quantize_fp8
 
-from gpu_common import (FP8_TOL, check_dispatch, check_expert_rows, check_outputs, gpu_run, log,
-                        oracle_run, sample_tokens)
+from gpu_common import (FP8_TOL, CachedWeights, check_dispatch, check_expert_rows, check_outputs,
+                        gpu_run, log, oracle_run, poison_workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -38,21 +38,22 @@ def test_quantizer_bit_exact(T, d, scale):
         list(zip(*bad))[:5], got_q[bad][:5], codes[bad][:5])
 
 
-def _case(cfg, *, n_streams=1, tokens=None):
+def _case(cfg, *, n_streams=1):
+    """Every token and every Y_perm row against the oracle, with the
+    workspace poisoned with NaN before the run."""
     log("fp8 case %s: d=%d f=%d E=%d E_loc=%d k=%d lengths=%s shared=%d streams=%d" % (
         cfg.name, cfg.d, cfg.f, cfg.E, cfg.E_loc, cfg.k, cfg.lengths, cfg.has_shared, n_streams))
     w = inputs.make_weights(cfg, "cuda")
     mbs = inputs.make_microbatches(cfg, "cuda")
-    ow = oracle.OracleWeights(w, "fp8")
+    ow = CachedWeights(oracle.OracleWeights(w, "fp8"))
     streams = [torch.cuda.Stream() for _ in range(n_streams)] if n_streams > 1 else None
     Tmax = max(max(mb.ids.shape[0] for mb in mbs), 1)
     with ExpertStage(cfg, w, n_slots=len(mbs), max_tokens=Tmax) as st:
+        poison_workspace(st)
         outs, slots, _ = gpu_run(st, mbs, streams=streams)
         errs = []
         for mb, ob, sl in zip(mbs, outs, slots):
-            T = mb.ids.shape[0]
-            tok = None if tokens is None else sample_tokens(T, tokens)
-            ref = oracle_run(cfg, ow, mb, tokens=tok)
+            ref = oracle_run(cfg, ow, mb)
             view = st.view(sl)
             check_dispatch(view, ref, cfg, mb)
             errs.append(check_outputs(ob, ref, FP8_TOL, cfg.name))
@@ -80,4 +81,12 @@ def test_fp8_shared_expert():
 
 
 def test_c4_fp8_skewed_four_streams():
-    _case(inputs.CONFIGS["c4"], n_streams=4, tokens=48)
+    _case(inputs.CONFIGS["c4"], n_streams=4)
+
+
+def test_fp8_many_row_tiles_per_group():
+    """fp8 with 13-14 row tiles per expert (bands of 4 row tiles, several
+    bands per group) and more tiles than CUs; d = 1024, f = 512, about 26k
+    routed rows; every row is checked."""
+    _case(inputs.MoEConfig("f8band", d=1024, f=512, E=16, e0=0, E_loc=8, k=8, lengths=(6500,),
+                           dtype="fp8", seed=21))

@@ -13,28 +13,29 @@ from paper_2606_22541_amd import inputs
 from paper_2606_22541_amd import moe_stage as C
 from paper_2606_22541_amd.stage import ExpertStage, bf16_bits, to_device_routing
 
-from gpu_common import (BF16_TOL, check_dispatch, check_expert_rows, check_outputs, gpu_run, log,
-                        oracle_run, sample_tokens)
+from gpu_common import (BF16_TOL, CachedWeights, band_order_tiles, check_dispatch, check_expert_rows,
+                        check_outputs, gpu_run, log, oracle_run, poison_workspace)
 
 pytestmark = pytest.mark.gpu
 
 
-def _case(cfg, mbs=None, *, n_streams=1, tokens=None, mode=0, tol=BF16_TOL, n_slots=None):
+def _case(cfg, mbs=None, *, n_streams=1, mode=0, tol=BF16_TOL, n_slots=None):
+    """Every token and every Y_perm row of every micro-batch against the
+    oracle, with the workspace poisoned with NaN before the run."""
     log("case %s: d=%d f=%d E=%d E_loc=%d k=%d lengths=%s shared=%d streams=%d" % (
         cfg.name, cfg.d, cfg.f, cfg.E, cfg.E_loc, cfg.k, cfg.lengths, cfg.has_shared, n_streams))
     w = inputs.make_weights(cfg, "cuda")
     if mbs is None:
         mbs = inputs.make_microbatches(cfg, "cuda")
-    ow = oracle.OracleWeights(w, cfg.dtype)
+    ow = CachedWeights(oracle.OracleWeights(w, cfg.dtype))
     streams = [torch.cuda.Stream() for _ in range(n_streams)] if n_streams > 1 else None
     with ExpertStage(cfg, w, n_slots=n_slots or len(mbs),
                      max_tokens=max(max(mb.ids.shape[0] for mb in mbs), 1)) as st:
+        poison_workspace(st)
         outs, slots, keep = gpu_run(st, mbs, streams=streams, mode=mode)
         errs = []
         for mb, ob, sl in zip(mbs, outs, slots):
-            T = mb.ids.shape[0]
-            tok = tokens if tokens is None else sample_tokens(T, tokens)
-            ref = oracle_run(cfg, ow, mb, tokens=tok)
+            ref = oracle_run(cfg, ow, mb)
             view = st.view(sl)
             check_dispatch(view, ref, cfg, mb)
             errs.append(check_outputs(ob, ref, tol, cfg.name))
@@ -129,9 +130,39 @@ def test_host_errors_enqueue_nothing():
         with pytest.raises(C.MoEStageError):                  # bad combine mode
             C.moe_dispatch(st.handle, 0, C.make_microbatch(2, x, ids, wt, out, combine_mode=7))
         assert C.moe_stage_sync_status(st.handle) == C.MOE_OK
-    bad = C.make_desc(200, 128, 8, 0, 4, 2, 4)                # d not a multiple of 128
-    with pytest.raises(C.MoEStageError):
+    for dd, ff in ((200, 128), (256, 192)):                    # d or f not a multiple of 128
+        bad = C.make_desc(dd, ff, 8, 0, 4, 2, 4)
+        with pytest.raises(C.MoEStageError) as e:
+            C.moe_stage_create(bad, C.make_weights(w.w_gate, w.w_up, w.w_down))
+        assert e.value.status == C.MOE_EUNSUPPORTED
+    bad = C.make_desc(256, 128, 8, 6, 4, 2, 4)                # local experts past n_experts
+    with pytest.raises(C.MoEStageError) as e:
         C.moe_stage_create(bad, C.make_weights(w.w_gate, w.w_up, w.w_down))
+    assert e.value.status == C.MOE_EINVAL
+
+
+def test_poll_reports_busy_then_done():
+    """moe_stage_poll never waits: a slot is MOE_OK before its first use,
+    MOE_OK or MOE_EBUSY while a micro-batch runs, and MOE_OK once it is done."""
+    cfg = inputs.CONFIGS["c1"]
+    w = inputs.make_weights(cfg, "cuda")
+    mbs = inputs.make_microbatches(cfg, "cuda")
+    with ExpertStage(cfg, w, n_slots=2) as st:
+        assert C.moe_stage_poll(st.handle, 0) == C.MOE_OK
+        assert C.moe_stage_poll(st.handle, 1) == C.MOE_OK
+        with pytest.raises(C.MoEStageError):
+            C.moe_stage_poll(st.handle, 2)
+        ids, wt = to_device_routing(mbs[0].ids, mbs[0].w)
+        out = torch.empty((4096, cfg.d), dtype=torch.bfloat16, device="cuda")
+        torch.cuda.synchronize()
+        seen = set()
+        for _ in range(4):                       # four micro-batches, ~0.2 ms each
+            slot = st.submit(st.microbatch(mbs[0].x, ids, wt, out))
+            seen.add(C.moe_stage_poll(st.handle, slot))
+        log("  poll right after submit: %s" % sorted(seen))
+        st.sync()
+        assert C.moe_stage_poll(st.handle, 0) == C.MOE_OK
+        assert C.moe_stage_poll(st.handle, 1) == C.MOE_OK
 
 
 def test_accumulate_mode_and_determinism():
@@ -195,22 +226,38 @@ def test_streams_match_single_stream_bitwise():
 
 
 # ---------------------------------------------------------------------------
-# Full-size configurations (outputs checked on sampled tokens)
+# Full-size configurations (every token and every routed row checked)
 # ---------------------------------------------------------------------------
 def test_c1_deepseek_ep32_share():
-    _case(inputs.CONFIGS["c1"], tokens=96)
+    _case(inputs.CONFIGS["c1"])
 
 
 def test_c1p_deepseek_ep32_share_32k_tokens():
-    _case(inputs.CONFIGS["c1p"], tokens=64)
+    _case(inputs.CONFIGS["c1p"])
 
 
 def test_c2_skewed_four_streams():
-    _case(inputs.CONFIGS["c2"], n_streams=4, tokens=48)
+    _case(inputs.CONFIGS["c2"], n_streams=4)
 
 
 def test_c3_ep8_share_with_shared_expert():
-    _case(inputs.CONFIGS["c3"], tokens=48)
+    _case(inputs.CONFIGS["c3"])
+
+
+def test_band_order_with_more_tiles_than_cus():
+    """More 256x256 tiles than CUs with a last round more than half full: the
+    256-row GEMMs keep the band order (row tiles rastered in bands of 4 per
+    column block, partial tiles beside their full ones) in both products.
+    d = 1024, f = 512 and about 26k routed rows over 8 experts (13-14 row
+    tiles each); every row is checked."""
+    cfg = inputs.MoEConfig("band", d=1024, f=512, E=16, e0=0, E_loc=8, k=8, lengths=(6500,), seed=21)
+    mbs = inputs.make_microbatches(cfg, "cuda")
+    disp = oracle.dispatch(mbs[0].ids, cfg.E, cfg.e0, cfg.E_loc)
+    for N, small in ((2 * cfg.f, 192), (cfg.d, 0)):       # gate/up, down (every group)
+        total, cus, by_size = band_order_tiles(disp["counts"][:cfg.E_loc], N, small)
+        log("  N=%d: %d tiles on %d CUs, size order %s" % (N, total, cus, by_size))
+        assert not by_size, "the case no longer exercises the band order"
+    _case(cfg, mbs)
 
 
 def test_max_local_experts_and_group_size_boundaries():

@@ -176,46 +176,53 @@ def test_token_permutation_equivariance():
     assert np.array_equal(b, a[perm])
 
 
-def test_fp8_stage_is_bf16_stage_on_dequantised_operands():
+def test_fp8_stage_brute_force():
     """fp8: x and W enter through their e4m3 values times scales, and h is
-    quantised per 128 channels before the down projection."""
+    quantised per row and 128 channels from its fp32 value before the down
+    projection.  Checked against a pure-Python rebuild whose quantiser scans
+    every e4m3 code (no oracle helper), with two 128-blocks along d so that a
+    transposed block scale fails.  A bf16 rounding of h before quantising
+    flips about one code in 60 here and fails too."""
+    from brute_force import bf_quantize_dequantize, bf_swiglu_fp8
     rng = np.random.default_rng(12)
-    T, d, f, E, k = 6, 256, 128, 4, 2
+    T, d, f, E, k, E_loc = 4, 256, 128, 3, 2, 2
     x_bits = _bf16_round(rng.standard_normal((T, d)))
     ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
     w = rng.random((T, k)).astype(np.float32)
     codes = [rng.integers(0, 0x7E, size=s).astype(np.uint8) | (rng.integers(0, 2, size=s).astype(np.uint8) << 7)
-             for s in ((2, f, d), (2, f, d), (2, d, f))]
+             for s in ((E_loc, f, d), (E_loc, f, d), (E_loc, d, f))]
     scales = [np.abs(rng.standard_normal(s)).astype(np.float32) * 1e-3 + 1e-4
-              for s in ((2, f // 128, d // 128), (2, f // 128, d // 128), (2, d // 128, f // 128))]
-
-    class Wt:
-        gate, up, down = (codes[0], scales[0]), (codes[1], scales[1]), (codes[2], scales[2])
-
-    ow = oracle.OracleWeights.__new__(oracle.OracleWeights)
-    ow.dtype, ow.gate, ow.up, ow.down, ow.sh = "fp8", Wt.gate, Wt.up, Wt.down, None
-    cfg = _cfg(d=d, f=f, E=E, e0=0, E_loc=2, k=k, dtype="fp8")
+              for s in ((E_loc, f // 128, d // 128), (E_loc, f // 128, d // 128), (E_loc, d // 128, f // 128))]
+    wts = SimpleNamespace(w_gate=codes[0], w_up=codes[1], w_down=codes[2],
+                          s_gate=scales[0], s_up=scales[1], s_down=scales[2], sh_gate=None)
+    ow = oracle.OracleWeights(wts, "fp8")
+    cfg = _cfg(d=d, f=f, E=E, e0=0, E_loc=E_loc, k=k, dtype="fp8")
     res = oracle.run_stage(cfg, ow, x_bits, ids, w)
-    # rebuild by hand: dequantised x, dequantised W, quantised h
-    xq, xs = oracle.quantize_groups(oracle.bf16_bits_to_f32(x_bits))
-    x = oracle.e4m3_decode(xq) * np.repeat(xs, 128, axis=1)
-    out = np.zeros((T, d))
+
+    vals = bf_e4m3_table()
+
+    def deq(c, s, e):
+        R, Cn = c.shape[1], c.shape[2]
+        return [[vals[int(c[e, i, j])] * float(s[e, i // 128, j // 128]) for j in range(Cn)] for i in range(R)]
+
+    xf = [[float(v) for v in row] for row in oracle.bf16_bits_to_f32(x_bits)]
+    xd = [bf_quantize_dequantize(row) for row in xf]
+    W = [tuple(deq(codes[m], scales[m], e) for m in range(3)) for e in range(E_loc)]
     for t in range(T):
+        want = [0.0] * d
         for j in range(k):
-            e = ids[t, j]
-            if e >= 2:
-                continue
-            Wg = oracle.e4m3_decode(codes[0][e]) * np.kron(scales[0][e], np.ones((128, 128)))
-            Wu = oracle.e4m3_decode(codes[1][e]) * np.kron(scales[1][e], np.ones((128, 128)))
-            Wd = oracle.e4m3_decode(codes[2][e]) * np.kron(scales[2][e], np.ones((128, 128)))
-            g = Wg @ x[t]
-            h = (g / (1 + np.exp(-g))) * (Wu @ x[t])
-            hb = torch.from_numpy(h[None, :].astype(np.float32)).to(torch.bfloat16).float().numpy()
-            hq, hs = oracle.quantize_groups(hb)
-            hd = oracle.e4m3_decode(hq[0]) * np.repeat(hs[0], 128)
-            out[t] += w[t, j] * (Wd @ hd)
-    np.testing.assert_allclose(res["out"], out, rtol=1e-12, atol=1e-12)
-    assert np.array_equal(res["x_codes"], xq)
+            e = int(ids[t, j])
+            if e < E_loc:
+                y = bf_swiglu_fp8(xd[t], *W[e])
+                want = [a + float(w[t, j]) * b for a, b in zip(want, y)]
+        np.testing.assert_allclose(res["out"][t], want, rtol=1e-12, atol=1e-12)
+
+
+def bf_e4m3_table():
+    """All 256 E4M3FN codes decoded from sign, exponent and mantissa fields."""
+    from brute_force import bf_e4m3_values
+    pos = bf_e4m3_values() + [float("nan")]
+    return pos + [-v for v in pos]
 
 
 def test_grouped_counts_reading():
@@ -264,3 +271,102 @@ def test_grouped_rows_equal_the_dispatched_rows(dtype):
     g = oracle.run_grouped(cfg, _W(experts), rows, counts)
     assert g["counts"].tolist() == counts.tolist()
     np.testing.assert_array_equal(g["y"], res["y"])
+
+
+def test_rel_l2_hand_values():
+    """rel_l2 = ||a - ref||_2 / ||ref||_2 over all elements, worked by hand."""
+    assert oracle.rel_l2(np.array([1.1, 0.0]), np.array([1.0, 0.0])) == pytest.approx(0.1, rel=1e-12)
+    # |a - ref| = 2, |ref| = 1: 2 (dividing by |a| = 3 would give 2/3; no sqrt gives 4)
+    assert oracle.rel_l2(np.array([3.0, 0.0]), np.array([1.0, 0.0])) == pytest.approx(2.0, rel=1e-15)
+    # a 3-4-5 triangle: |a - ref| = 5, |ref| = sqrt(4 + 4 + 1) = 3
+    assert oracle.rel_l2(np.array([5.0, 6.0, 1.0]), np.array([2.0, 2.0, 1.0])) == pytest.approx(5 / 3, rel=1e-15)
+    # the norm runs over every element of a matrix, not per row
+    a = np.array([[1.0, 0.0], [0.0, 1.0]])
+    ref = np.array([[1.0, 0.0], [0.0, 0.0]])
+    assert oracle.rel_l2(a, ref) == pytest.approx(1.0, rel=1e-15)
+    assert oracle.rel_l2(2 * ref, ref) == pytest.approx(1.0, rel=1e-15)
+    # a zero reference: exact zeros pass, anything else is infinitely wrong
+    z = np.zeros((3, 4))
+    assert oracle.rel_l2(z, z) == 0.0
+    assert oracle.rel_l2(z + 1e-30, z) == float("inf")
+    # symmetric in the sign of the error, scale-invariant
+    r = np.random.default_rng(0).standard_normal(50)
+    e = np.random.default_rng(1).standard_normal(50) * 1e-3
+    assert oracle.rel_l2(r + e, r) == pytest.approx(oracle.rel_l2(r - e, r), rel=1e-12)
+    assert oracle.rel_l2(8 * (r + e), 8 * r) == pytest.approx(oracle.rel_l2(r + e, r), rel=1e-12)
+
+
+def _bf16_tensor(vals):
+    return torch.tensor(vals, dtype=torch.float32).to(torch.bfloat16)
+
+
+def test_oracle_weights_bf16_values_and_orientation():
+    """OracleWeights built from the checkpoint layout (torch bf16 tensors,
+    gate/up [E_loc][f][d], down [E_loc][d][f], shared with a leading 1):
+    every matrix keeps its own values and orientation, and the whole stage
+    with these weights equals the brute force on the same values."""
+    E_loc, f, d = 2, 3, 5
+    gate = [[[e * 16 + i * 5 + j + 1 for j in range(d)] for i in range(f)] for e in range(E_loc)]
+    up = [[[-(e * 16 + i * 5 + j + 1) / 4 for j in range(d)] for i in range(f)] for e in range(E_loc)]
+    down = [[[(e * 16 + i * 3 + j + 1) / 8 for j in range(f)] for i in range(d)] for e in range(E_loc)]
+    shg = [[[(i * 5 + j + 1) / 16 for j in range(d)] for i in range(f)]]
+    shu = [[[(i * 5 + j + 2) / 32 for j in range(d)] for i in range(f)]]
+    shd = [[[-(i * 3 + j + 1) / 64 for j in range(f)] for i in range(d)]]
+    w = SimpleNamespace(w_gate=_bf16_tensor(gate), w_up=_bf16_tensor(up), w_down=_bf16_tensor(down),
+                        sh_gate=_bf16_tensor(shg), sh_up=_bf16_tensor(shu), sh_down=_bf16_tensor(shd))
+    ow = oracle.OracleWeights(w, "bf16")
+    for e in range(E_loc):
+        g, u, dn = ow.expert(e)
+        assert g.shape == (f, d) and u.shape == (f, d) and dn.shape == (d, f)
+        assert g.dtype == np.float64
+        assert np.array_equal(g, np.array(gate[e])) and np.array_equal(u, np.array(up[e]))
+        assert np.array_equal(dn, np.array(down[e]))
+    sg, su, sd = ow.shared()
+    assert np.array_equal(sg, np.array(shg[0])) and np.array_equal(su, np.array(shu[0]))
+    assert np.array_equal(sd, np.array(shd[0])) and sd.shape == (d, f)
+    # end to end: a swapped gate/up or a transposed matrix changes these outputs
+    rng = np.random.default_rng(5)
+    T, E, k = 5, 3, 2
+    x_bits = _bf16_round(rng.standard_normal((T, d)) * 0.1)
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    wt = rng.random((T, k)).astype(np.float32)
+    cfg = _cfg(d=d, f=f, E=E, e0=1, E_loc=E_loc, k=k, has_shared=True)
+    res = oracle.run_stage(cfg, ow, x_bits, ids, wt)
+    want = bf_stage(oracle.bf16_bits_to_f64(x_bits).tolist(), ids.tolist(),
+                    wt.astype(np.float64).tolist(),
+                    [(gate[e], up[e], down[e]) for e in range(E_loc)], E, 1, E_loc,
+                    shared=(shg[0], shu[0], shd[0]))
+    np.testing.assert_allclose(res["out"], np.array(want), rtol=1e-12, atol=1e-12)
+
+
+def test_oracle_weights_fp8_block_scales():
+    """fp8 weights: code values times the scale of their 128x128 block,
+    scales indexed [E_loc][rows/128][cols/128] (distinct powers of two, so a
+    transposed or shifted block index gives other values)."""
+    E_loc, f, d = 2, 128, 256
+    rng = np.random.default_rng(6)
+    mk = lambda s: (rng.integers(0, 0x7E, size=s).astype(np.uint8) |
+                    (rng.integers(0, 2, size=s).astype(np.uint8) << 7))
+    cg, cu, cd = mk((E_loc, f, d)), mk((E_loc, f, d)), mk((E_loc, d, f))
+    sg = np.array([[[2.0 ** -(e * 8 + bj + 1) for bj in range(2)]] for e in range(E_loc)], np.float32)
+    su = np.array([[[2.0 ** -(e * 8 + bj + 3) for bj in range(2)]] for e in range(E_loc)], np.float32)
+    sd = np.array([[[2.0 ** -(e * 8 + bi + 5)] for bi in range(2)] for e in range(E_loc)], np.float32)
+    shc = [mk((1, f, d)), mk((1, f, d)), mk((1, d, f))]
+    shs = [np.array([[[0.5, 0.25]]], np.float32), np.array([[[0.125, 0.0625]]], np.float32),
+           np.array([[[3.0], [5.0]]], np.float32)]
+    w = SimpleNamespace(w_gate=torch.from_numpy(cg), w_up=torch.from_numpy(cu), w_down=torch.from_numpy(cd),
+                        s_gate=torch.from_numpy(sg), s_up=torch.from_numpy(su), s_down=torch.from_numpy(sd),
+                        sh_gate=shc[0], sh_up=shc[1], sh_down=shc[2],
+                        sh_s_gate=shs[0], sh_s_up=shs[1], sh_s_down=shs[2])
+    ow = oracle.OracleWeights(w, "fp8")
+    vals = bf_e4m3_table()
+    for e in range(E_loc):
+        g, u, dn = ow.expert(e)
+        assert g.shape == (f, d) and dn.shape == (d, f)
+        for (i, j) in [(0, 0), (5, 130), (127, 255), (64, 127)]:
+            assert g[i, j] == vals[cg[e, i, j]] * 2.0 ** -(e * 8 + j // 128 + 1)
+            assert u[i, j] == vals[cu[e, i, j]] * 2.0 ** -(e * 8 + j // 128 + 3)
+            assert dn[j, i] == vals[cd[e, j, i]] * 2.0 ** -(e * 8 + j // 128 + 5)
+    g, u, dn = ow.shared()
+    assert g[3, 200] == vals[shc[0][0, 3, 200]] * 0.25 and u[3, 7] == vals[shc[1][0, 3, 7]] * 0.125
+    assert dn[200, 3] == vals[shc[2][0, 200, 3]] * 5.0 and dn[7, 3] == vals[shc[2][0, 7, 3]] * 3.0
