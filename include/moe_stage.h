@@ -280,6 +280,33 @@ MOE_API moe_status moe_ingest_signal(uint32_t *word, uint32_t epoch, void *strea
  * whether the next submit would make its stream wait. */
 MOE_API moe_status moe_stage_poll(moe_stage *stage, int32_t slot);
 
+/* The dispatch index of moe_dispatch (histogram over all experts, offsets,
+ * stable counting-sort permutation; bf16 moe_dispatch minus the stage) for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  Allocates nothing:
+ * its only scratch (one histogram row of n_experts counts per 1024 slots,
+ * and the grouped-GEMM tile tables) is a fixed 4 MiB array that the library
+ * holds on every device it runs on until the process ends.
+ * Inputs:  topk_ids [n_tokens][top_k] int32 (-1 = masked), device memory.
+ * Outputs (device memory, written as moe_dispatch writes them into a slot):
+ *   counts [n_experts], offsets [n_local_experts + 1],
+ *   slot_of_row [n_tokens * top_k] (the first offsets[n_local_experts]
+ *   entries are written), row_of_slot [n_tokens * top_k].
+ * err: optional device int32; an expert id outside [-1, n_experts) sets
+ *   bit 0 (the slot is skipped); the caller clears it.  NULL: not reported.
+ * Errors: MOE_EINVAL for bad sizes or null pointers; MOE_EUNSUPPORTED when
+ * ceil(n_tokens * top_k / 1024) * n_experts > 2^20 (the scratch holds no
+ * more histogram rows); nothing is enqueued then.  Every call on a device
+ * shares that device's scratch array: calls that overlap on one device
+ * (two streams, two threads) race and must be serialised by the caller.
+ * `stream` must belong to the current device. */
+MOE_API moe_status moe_dispatch_index_noalloc(const int32_t *topk_ids, int32_t n_tokens,
+                                              int32_t top_k, int32_t n_experts,
+                                              int32_t first_local_expert, int32_t n_local_experts,
+                                              int32_t *counts, int32_t *offsets,
+                                              int32_t *slot_of_row, int32_t *row_of_slot,
+                                              int32_t *err, void *stream);
+
 /* Fills `out` with the device pointers of `slot`'s workspace. */
 MOE_API moe_status moe_stage_query(moe_stage *stage, int32_t slot, moe_dispatch_view *out);
 

@@ -39,7 +39,7 @@ EXPORTS = (
     "moe_stage_submit_microbatch", "moe_quantize_fp8", "moe_stage_query", "moe_stage_sync",
     "moe_stage_workspace_bytes", "moe_status_string", "moe_stage_profile",
     "moe_stage_profile_read", "moe_ingest_wait", "moe_ingest_signal", "moe_expert_ffn_grouped",
-    "moe_stage_poll",
+    "moe_stage_poll", "moe_dispatch_index_noalloc",
 )
 MOE_PROF_KINDS = 6
 PROF_KIND_NAMES = ("dispatch_index", "gather", "gemm_gate_up_swiglu", "gemm_down", "combine",
@@ -110,6 +110,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "moe_stage_query": (st, [P, ctypes.c_int32, ctypes.POINTER(moe_dispatch_view)]),
         "moe_stage_sync": (st, [P]),
         "moe_stage_poll": (st, [P, ctypes.c_int32]),
+        "moe_dispatch_index_noalloc": (st, [P] + [ctypes.c_int32] * 5 + [P] * 6),
         "moe_stage_workspace_bytes": (st, [ctypes.POINTER(moe_stage_desc),
                                            ctypes.POINTER(ctypes.c_int64)]),
         "moe_status_string": (ctypes.c_char_p, [st]),
@@ -243,6 +244,16 @@ def moe_stage_poll(stage: int, slot: int) -> int:
     if r not in (MOE_OK, MOE_EBUSY):
         raise MoEStageError(r, "moe_stage_poll")
     return r
+
+
+def moe_dispatch_index_noalloc(topk_ids, n_tokens: int, top_k: int, n_experts: int,
+                               first_local_expert: int, n_local_experts: int, counts, offsets,
+                               slot_of_row, row_of_slot, err=None, stream=None) -> None:
+    """The dispatch index into caller-owned outputs, with no allocation."""
+    _check(load_library().moe_dispatch_index_noalloc(
+        _ptr(topk_ids), n_tokens, top_k, n_experts, first_local_expert, n_local_experts,
+        _ptr(counts), _ptr(offsets), _ptr(slot_of_row), _ptr(row_of_slot), _ptr(err),
+        _stream(stream)), "moe_dispatch_index_noalloc")
 
 
 def moe_stage_sync(stage: int) -> None:
