@@ -28,13 +28,26 @@ CFLAGS = [
 ]
 
 
+# Per-file additions.  The fp8 GEMM's inner loop interleaves one K group's
+# MFMAs and fp32 promotion with the next group's operand reads; the ILP
+# scheduling strategy keeps them interleaved instead of pairing each MFMA
+# with its own promotion and padding the gap with wait states.
+FILE_FLAGS = {
+    "gemm_fp8.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+}
+
+
+def flags_for(src: str):
+    return CFLAGS + FILE_FLAGS.get(os.path.basename(src), [])
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + CFLAGS + ["-c", src, "-o", obj]
+    cmd = [HIPCC] + flags_for(src) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr))

@@ -23,7 +23,7 @@ GEMMS = ("gemm_bf16.hip", "gemm_bf16_small.hip", "gemm_fp8.hip")
 
 
 def _asm(src):
-    cmd = [build.HIPCC] + [f for f in build.CFLAGS if f != "-fPIC"] + [
+    cmd = [build.HIPCC] + [f for f in build.flags_for(src) if f != "-fPIC"] + [
         "-S", "--offload-device-only", os.path.join(build.CSRC, src), "-o", "-"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
