@@ -19,6 +19,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -452,6 +453,112 @@ def run_triple_stream(name="c1", in_flight=3, steps=40, warmup=30, repeats=3):
             "ms_per_microbatch": round(best, 4), "tokens_per_s": round(T / (best / 1e3), 1)}
 
 
+# CU partitions of the three-stream layout (section 3.4.1 gives compute and
+# each communication stream its own share of the cores): name -> per stream
+# (first CU, CU count) as a function of the device's CU count.
+CU_PARTITIONS = {
+    "all_cus": lambda n: {"dispatch": (0, n), "gemm": (0, n), "combine": (0, n)},
+    "split16": lambda n: {"dispatch": (0, 16), "combine": (16, 16), "gemm": (32, n - 32)},
+    "split32": lambda n: {"dispatch": (0, 32), "combine": (32, 32), "gemm": (64, n - 64)},
+    "gemm_all_16": lambda n: {"dispatch": (0, 16), "combine": (16, 16), "gemm": (0, n)},
+}
+
+
+def run_cu_partition_child(partition, name="c1", in_flight=3, steps=40, warmup=30, repeats=3):
+    """The three-stream layout of run_triple_stream on CU-masked streams, in
+    a process where nothing else created a stream: each masked stream takes
+    a hardware queue of its own (the runtime gives a process four), so the
+    three are created first, through the library, and torch's work stays on
+    the null stream (events reach the masked streams through ExternalStream
+    wrappers)."""
+    import torch
+    from paper_2606_22541_amd import inputs
+    from paper_2606_22541_amd import moe_stage as C
+    from paper_2606_22541_amd.stage import ExpertStage, to_device_routing
+
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    C.load_library()
+    parts = CU_PARTITIONS[partition](cus)
+    hs = {k: C.moe_stream_create_cu_masked(*v) for k, v in parts.items()}
+    D, G, R = (torch.cuda.ExternalStream(hs[k]) for k in ("dispatch", "gemm", "combine"))
+    main = torch.cuda.current_stream()
+    cfg = inputs.CONFIGS[name]
+    w = inputs.make_weights(cfg, "cuda")
+    mb = inputs.make_microbatches(cfg, "cuda")[0]
+    T = mb.ids.shape[0]
+    ids, wt = to_device_routing(mb.ids, mb.w)
+    nb = in_flight + 1
+    xs = [mb.x.clone() for _ in range(nb)]
+    outs = [torch.empty((T, cfg.d), dtype=torch.bfloat16, device="cuda") for _ in range(nb)]
+    stage = ExpertStage(cfg, w, n_slots=nb, max_tokens=T)
+    del w
+    mbs = [stage.microbatch(xs[i], ids, wt, outs[i]) for i in range(nb)]
+    slot_done = [None] * nb
+    torch.cuda.synchronize()
+
+    def run(n):
+        go = torch.cuda.Event()
+        go.record(main)
+        for st_ in (D, G, R):
+            st_.wait_event(go)
+        for i in range(n):
+            k = i % nb
+            if slot_done[k] is not None:
+                D.wait_event(slot_done[k])
+            stage.dispatch(k, mbs[k], hs["dispatch"])
+            e1 = torch.cuda.Event()
+            e1.record(D)
+            G.wait_event(e1)
+            stage.expert_ffn(k, hs["gemm"])
+            e2 = torch.cuda.Event()
+            e2.record(G)
+            R.wait_event(e2)
+            stage.combine(k, hs["combine"])
+            e3 = torch.cuda.Event()
+            e3.record(R)
+            slot_done[k] = e3
+        e = torch.cuda.Event()
+        e.record(R)
+        main.wait_event(e)
+
+    run(warmup)
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(repeats):
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        start.record(main)
+        run(steps)
+        end.record(main)
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(end) / steps
+        best = ms if best is None else min(best, ms)
+    stage.sync()
+    torch.cuda.synchronize()
+    stage.close()
+    for h in hs.values():
+        C.moe_stream_destroy(h)
+    return {"partition": partition,
+            "cus": {k: list(v) for k, v in parts.items()},
+            "ms_per_microbatch": round(best, 4), "tokens_per_s": round(T / (best / 1e3), 1)}
+
+
+def run_cu_partition(name="c1", partitions=("all_cus", "split16", "split32", "gemm_all_16")):
+    """CU-partitioned three-stream layouts, each measured in a child process
+    of its own (a fresh budget of hardware queues)."""
+    res = []
+    for part in partitions:
+        r = subprocess.run([sys.executable, os.path.abspath(__file__), "--cu-partition-child", part,
+                            "--workload", name], capture_output=True, text=True, timeout=300)
+        if r.returncode != 0:
+            res.append({"partition": part, "error": r.stderr.strip().splitlines()[-1:]})
+            continue
+        res.append(json.loads(r.stdout.strip().splitlines()[-1]))
+        _log("[bench] cu partition %s done" % part)
+    return {"workload": "%s micro-batches, dispatch / grouped GEMMs / combine on three CU-masked "
+                        "streams, up to 4 micro-batches in flight" % name, "layouts": res}
+
+
 def run_ingest(name="c1", senders=4, rounds=20, warmup=5):
     """Asynchronous ingest (section 3.2.1): each round, `senders` senders copy
     their share of a micro-batch (token rows, ids, weights) into the stage's
@@ -847,6 +954,10 @@ def main():
                     help="skip the latency-vs-tokens sweep of the c1 expert share")
     ap.add_argument("--layers", type=int, default=8,
                     help="layers for the layer-oblivious dispatch measurement (0: skip)")
+    ap.add_argument("--cu-partition", type=int, default=1,
+                    help="also time the three-stream layout on CU-masked streams (0: skip)")
+    ap.add_argument("--cu-partition-child", default="",
+                    help="internal: measure one CU partition in this (fresh) process and exit")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -858,6 +969,9 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.cu_partition_child:
+        print(json.dumps(run_cu_partition_child(args.cu_partition_child, args.workload)), flush=True)
+        return
     if args.calibrate_copy_mib:
         n = args.calibrate_copy_mib << 20
         src = torch.ones(n, dtype=torch.uint8, device="cuda")
@@ -924,6 +1038,8 @@ def main():
     if args.grouped:
         line["%s_grouped" % args.workload] = run_grouped(args.workload)
         _log("[bench] grouped %s done" % args.workload)
+    if args.cu_partition:
+        line["%s_cu_partition" % args.workload] = run_cu_partition(args.workload)
     if not args.no_sweep:
         line["token_sweep"] = run_sweep()
         _log("[bench] token sweep done")

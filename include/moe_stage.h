@@ -307,6 +307,20 @@ MOE_API moe_status moe_dispatch_index_noalloc(const int32_t *topk_ids, int32_t n
                                               int32_t *slot_of_row, int32_t *row_of_slot,
                                               int32_t *err, void *stream);
 
+/* A stream whose kernels may run only on the current device's compute units
+ * [first_cu, first_cu + n_cus) (mask bits in the runtime's CU order), so
+ * dispatch and combine can be given their own share of the CUs beside the
+ * grouped GEMMs (section 3.4.1: compute and communication streams each own
+ * a partition of the cores).  The stage's persistent kernels size their
+ * grids by the CUs of the stream they are launched on.  Each such stream
+ * takes a hardware queue of its own: with the runtime's default of four
+ * queues per process, create at most three, before any other stream.
+ * MOE_EINVAL for a null out or a range outside the device; MOE_ENOMEM when
+ * no hardware queue is left.  Destroy with moe_stream_destroy, which waits
+ * for the stream's work first. */
+MOE_API moe_status moe_stream_create_cu_masked(int32_t first_cu, int32_t n_cus, void **stream_out);
+MOE_API moe_status moe_stream_destroy(void *stream);
+
 /* Fills `out` with the device pointers of `slot`'s workspace. */
 MOE_API moe_status moe_stage_query(moe_stage *stage, int32_t slot, moe_dispatch_view *out);
 

@@ -736,6 +736,35 @@ moe_status moe_quantize_fp8(const void *x_bf16, int32_t T, int32_t d, void *x_q,
     return MOE_OK;
 }
 
+moe_status moe_stream_create_cu_masked(int32_t first_cu, int32_t n_cus, void **stream_out)
+{
+    if (!stream_out) return MOE_EINVAL;
+    *stream_out = nullptr;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return MOE_EHIP;
+    if (first_cu < 0 || n_cus < 1 || first_cu + n_cus > cus || cus > 32 * 32) return MOE_EINVAL;
+    uint32_t mask[32] = {};
+    for (int c = first_cu; c < first_cu + n_cus; ++c) mask[c >> 5] |= 1u << (c & 31);
+    const uint32_t words = (uint32_t)((cus + 31) / 32);
+    hipStream_t s = nullptr;
+    const hipError_t e = hipExtStreamCreateWithCUMask(&s, words, mask);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return e == hipErrorOutOfMemory ? MOE_ENOMEM : MOE_EHIP;
+    }
+    *stream_out = (void *)s;
+    return MOE_OK;
+}
+
+moe_status moe_stream_destroy(void *stream)
+{
+    if (!stream) return MOE_EINVAL;
+    if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return MOE_EHIP;
+    return hipStreamDestroy((hipStream_t)stream) == hipSuccess ? MOE_OK : MOE_EHIP;
+}
+
 moe_status moe_stage_poll(moe_stage *st, int32_t slot)
 {
     if (!slot_ok(st, slot)) return MOE_EINVAL;

@@ -39,7 +39,8 @@ EXPORTS = (
     "moe_stage_submit_microbatch", "moe_quantize_fp8", "moe_stage_query", "moe_stage_sync",
     "moe_stage_workspace_bytes", "moe_status_string", "moe_stage_profile",
     "moe_stage_profile_read", "moe_ingest_wait", "moe_ingest_signal", "moe_expert_ffn_grouped",
-    "moe_stage_poll", "moe_dispatch_index_noalloc",
+    "moe_stage_poll", "moe_dispatch_index_noalloc", "moe_stream_create_cu_masked",
+    "moe_stream_destroy",
 )
 MOE_PROF_KINDS = 6
 PROF_KIND_NAMES = ("dispatch_index", "gather", "gemm_gate_up_swiglu", "gemm_down", "combine",
@@ -110,6 +111,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "moe_stage_query": (st, [P, ctypes.c_int32, ctypes.POINTER(moe_dispatch_view)]),
         "moe_stage_sync": (st, [P]),
         "moe_stage_poll": (st, [P, ctypes.c_int32]),
+        "moe_stream_create_cu_masked": (st, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(P)]),
+        "moe_stream_destroy": (st, [P]),
         "moe_dispatch_index_noalloc": (st, [P] + [ctypes.c_int32] * 5 + [P] * 6),
         "moe_stage_workspace_bytes": (st, [ctypes.POINTER(moe_stage_desc),
                                            ctypes.POINTER(ctypes.c_int64)]),
@@ -254,6 +257,18 @@ def moe_dispatch_index_noalloc(topk_ids, n_tokens: int, top_k: int, n_experts: i
         _ptr(topk_ids), n_tokens, top_k, n_experts, first_local_expert, n_local_experts,
         _ptr(counts), _ptr(offsets), _ptr(slot_of_row), _ptr(row_of_slot), _ptr(err),
         _stream(stream)), "moe_dispatch_index_noalloc")
+
+
+def moe_stream_create_cu_masked(first_cu: int, n_cus: int) -> int:
+    """A hipStream_t (as an int) restricted to CUs [first_cu, first_cu + n_cus)."""
+    h = ctypes.c_void_p()
+    _check(load_library().moe_stream_create_cu_masked(first_cu, n_cus, ctypes.byref(h)),
+           "moe_stream_create_cu_masked")
+    return h.value
+
+
+def moe_stream_destroy(stream: int) -> None:
+    _check(load_library().moe_stream_destroy(stream), "moe_stream_destroy")
 
 
 def moe_stage_sync(stage: int) -> None:

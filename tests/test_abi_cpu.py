@@ -129,4 +129,6 @@ def test_null_arguments_rejected_without_gpu(lib):
     assert lib.moe_expert_ffn_grouped(None, 0, ctypes.byref(gb), None) == C.MOE_EINVAL
     assert lib.moe_stage_create(None, None, None) == C.MOE_EINVAL
     assert lib.moe_stage_poll(None, 0) == C.MOE_EINVAL
+    assert lib.moe_stream_create_cu_masked(0, 16, None) == C.MOE_EINVAL
+    assert lib.moe_stream_destroy(None) == C.MOE_EINVAL
     lib.moe_stage_destroy(None)

@@ -110,3 +110,17 @@ def test_step_roofline_of_overlapped_micro_batches():
     ro8 = bench.step_roofline(r8)
     assert ro8["peak"] == bench.PEAK_FP8_TFLOPS
     assert ro8["algorithmic_bytes"] == 1e9 + 0.5e9 + 1e6 + 2e8 + 1e8  # fp8 gathers X_perm
+
+
+def test_cu_partitions_fit_the_device():
+    """Every CU partition of the three-stream ablation lies inside the
+    device's CUs; the split layouts give the three streams disjoint sets."""
+    for n in (256, 304, 80):
+        for name, f in bench.CU_PARTITIONS.items():
+            parts = f(n)
+            assert set(parts) == {"dispatch", "gemm", "combine"}
+            for first, cnt in parts.values():
+                assert 0 <= first and cnt >= 1 and first + cnt <= n
+            if name.startswith("split"):
+                sets = [set(range(a, a + c)) for a, c in parts.values()]
+                assert not (sets[0] & sets[1]) and not (sets[0] & sets[2]) and not (sets[1] & sets[2])
