@@ -44,8 +44,8 @@ NAME_MAP = (
     ("void moe::k_gemm_bf16_small<true>", "gemm_gate_up_swiglu"),
     ("void moe::k_gemm_bf16<true>", "gemm_gate_up_swiglu"),
     ("void moe::k_gemm_bf16<false>", "gemm_down"),
-    ("void moe::k_gemm_fp8<true,", "gemm_gate_up_swiglu_fp8"),
-    ("void moe::k_gemm_fp8<false,", "gemm_down_fp8"),
+    ("void moe::k_gemm_fp8<true>", "gemm_gate_up_swiglu_fp8"),
+    ("void moe::k_gemm_fp8<false>", "gemm_down_fp8"),
     ("moe::k_combine", "combine"),
     ("void moe::k_gather", "gather"),
     ("moe::k_hist", "dispatch_index"),
@@ -149,6 +149,64 @@ def traffic(args):
     print(json.dumps(rec, indent=1, sort_keys=True))
 
 
+def overlap(path: str, steps_skip: int, steps_use: int):
+    """Per-step overlap of the stage's kernels in a --kernel-trace of a
+    workload whose micro-batches run on their own streams.  The stage's
+    dispatches, in issue order, are cut into steps of equal kernel count
+    (every step issues the same kernels); of those, `steps_use` steps after
+    the first `steps_skip` are reduced.  Per step: the span (first start to
+    last end), the sum of kernel durations, the busy time of each stream
+    (union of its kernels' intervals) and of the device (union of all), and
+    the sum per kernel group.  overlap = sum of durations / device busy time
+    (1: nothing ran concurrently)."""
+    rows = [r for r in csv.DictReader(open(_find_csv(path, "kernel_trace.csv")))
+            if kind_of(r["Kernel_Name"]) not in (None, "quantize_fp8")]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    streams = sorted({r["Stream_Id"] for r in rows})
+    # kernels per step: the number of dispatches between consecutive
+    # dispatches of the first kernel name seen on the first stream
+    first = rows[0]["Kernel_Name"]
+    idx = [i for i, r in enumerate(rows) if r["Kernel_Name"] == first and
+           r["Stream_Id"] == rows[0]["Stream_Id"]]
+    per_step = idx[1] - idx[0]
+
+    def union(iv):
+        iv = sorted(iv)
+        tot, cur_s, cur_e = 0, None, None
+        for s_, e_ in iv:
+            if cur_e is None or s_ > cur_e:
+                if cur_e is not None:
+                    tot += cur_e - cur_s
+                cur_s, cur_e = s_, e_
+            else:
+                cur_e = max(cur_e, e_)
+        return tot + (cur_e - cur_s if cur_e is not None else 0)
+
+    acc = collections.defaultdict(float)
+    n = 0
+    for st in range(steps_skip, steps_skip + steps_use):
+        chunk = rows[st * per_step:(st + 1) * per_step]
+        if len(chunk) < per_step:
+            break
+        iv = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in chunk]
+        acc["span_us"] += (max(e for _, e in iv) - min(s_ for s_, _ in iv)) / 1e3
+        acc["sum_kernels_us"] += sum(e - s_ for s_, e in iv) / 1e3
+        acc["device_busy_us"] += union(iv) / 1e3
+        for sid in streams:
+            acc["stream_%s_busy_us" % sid] += union(
+                [(int(r["Start_Timestamp"]), int(r["End_Timestamp"])) for r in chunk
+                 if r["Stream_Id"] == sid]) / 1e3
+        for r in chunk:
+            acc["group_%s_us" % kind_of(r["Kernel_Name"])] += (
+                int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        n += 1
+    out = {k: round(v / n, 2) for k, v in acc.items()}
+    out["steps"] = n
+    out["kernels_per_step"] = per_step
+    out["overlap"] = round(out["sum_kernels_us"] / out["device_busy_us"], 3)
+    return out
+
+
 # gfx950 MFMA accounting (checked against the kernels' own tile counts):
 # SQ_INSTS_MFMA counts one per MFMA instruction a wave issues, and a
 # v_mfma_f32_32x32x16_bf16 (32768 FLOP) adds 32 to SQ_VALU_MFMA_BUSY_CYCLES;
@@ -214,8 +272,14 @@ def main(argv=None):
     t.add_argument("--command", default="")
     m = sub.add_parser("mfma")
     m.add_argument("path")
+    o = sub.add_parser("overlap")
+    o.add_argument("path")
+    o.add_argument("--skip", type=int, default=20)
+    o.add_argument("--use", type=int, default=120)
     a = ap.parse_args(argv)
-    if a.cmd == "stats":
+    if a.cmd == "overlap":
+        print(json.dumps(overlap(a.path, a.skip, a.use), indent=1, sort_keys=True))
+    elif a.cmd == "stats":
         print(json.dumps(kernel_stats(a.path), indent=1, sort_keys=True))
     elif a.cmd == "mfma":
         print(json.dumps(mfma_util(a.path), indent=1, sort_keys=True))
