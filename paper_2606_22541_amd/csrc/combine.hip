@@ -18,6 +18,20 @@ namespace moe {
 constexpr int kCombineThreads = 256;
 constexpr int kUnroll = 4;
 
+// A 16-byte load that marks its line streaming (read once).  Used for the
+// shared expert's rows and, in accumulate mode, the old output rows: both are
+// read exactly once and at the EP8 share (T = 16384) they are 235 MB each,
+// more than the 256 MB last-level cache holds beside them.  The expert rows
+// (Y_perm) keep ordinary loads: the down GEMM has just written them and they
+// are often still cached (measured: streaming loads of Y_perm made the
+// combine of the EP32 share at T = 32768 5% slower, those of the shared rows
+// made the EP8 share's 10% faster).
+__device__ __forceinline__ uint4 nt_load(const uint4 *p)
+{
+    const u32x4 v = __builtin_nontemporal_load((const u32x4 *)p);
+    return *(const uint4 *)&v;
+}
+
 __device__ __forceinline__ void acc_row(float (&acc)[8], const uint4 &v, float wj)
 {
     const bf16 *vb = (const bf16 *)&v;
@@ -45,7 +59,7 @@ void k_combine(const uint4 *__restrict__ y, const uint4 *__restrict__ ysh,
             if (accumulate) {
                 uint4 o[kUnroll];
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) o[u] = orow[cc[u]];
+                for (int u = 0; u < kUnroll; ++u) o[u] = nt_load(&orow[cc[u]]);
                 __builtin_amdgcn_sched_barrier(0);   // all loads issued first
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) {
@@ -62,7 +76,7 @@ void k_combine(const uint4 *__restrict__ y, const uint4 *__restrict__ ysh,
             if (shrow) {
                 uint4 v[kUnroll];
 #pragma unroll
-                for (int u = 0; u < kUnroll; ++u) v[u] = shrow[cc[u]];
+                for (int u = 0; u < kUnroll; ++u) v[u] = nt_load(&shrow[cc[u]]);
                 __builtin_amdgcn_sched_barrier(0);   // all loads issued first
 #pragma unroll
                 for (int u = 0; u < kUnroll; ++u) acc_row(acc[u], v[u], 1.0f);
