@@ -8,8 +8,14 @@ the oracle comparison.  Work is always enqueued in dependency order (each
 sender round before the stage round that waits for it), so a wait can never
 be stuck behind its own producer in a shared hardware queue; the timeout test
 forces the give-up path from the host with a word that is never raised and a
-tiny spin limit, so every kernel still exits normally.
+tiny spin limit, so every kernel still exits normally.  The late-producer test
+is the one exception: it enqueues the late senders after the wait that waits
+for them (on another stream, once the other micro-batches are seen done); the
+wait's spin limit bounds it, so streams sharing a hardware queue would make
+that test fail, never hang.
 """
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -50,10 +56,12 @@ def _delay(stream, n=6):
     return a
 
 
-def _send(stream, mb, recv, ready, epoch):
-    """Sender g copies its T/D tokens, then raises ready[g] to `epoch`."""
+def _send(stream, mb, recv, ready, epoch, routing=None):
+    """Sender g copies its T/D tokens, then raises ready[g] to `epoch`.
+    `routing`: the micro-batch's device ids and weights, made beforehand
+    (else made here, with a synchronous copy from the host)."""
     x, ids, w = recv
-    sids, sw = to_device_routing(mb.ids, mb.w)
+    sids, sw = routing if routing is not None else to_device_routing(mb.ids, mb.w)
     per = T // D
     with torch.cuda.stream(stream):
         for g in range(D):
@@ -156,3 +164,61 @@ def test_wrapping_epochs():
         with pytest.raises(C.MoEStageError) as e:
             st.sync()
         assert e.value.status == C.MOE_ETIMEOUT
+
+
+def test_late_producer_does_not_hold_back_the_others():
+    """A micro-batch whose senders are late holds back only itself (section
+    3.2.1: a batch is taken when it is ready, in whatever order).  Micro-batch
+    A is submitted first, on its own stream, behind a wait on its ready words
+    whose senders are not enqueued yet; B and C are then sent and submitted on
+    a second stream.  B's and C's slots complete while A's is still busy --
+    a certainty, not a race: nothing can release A yet -- and only then are
+    A's senders enqueued.  All three match the oracle.  Every device wait is
+    bounded, so if A's wait held back B and C it would give up after its spin
+    limit and the test would fail with MOE_ETIMEOUT, every kernel exited."""
+    cfgs = [_cfg(50 + i) for i in range(3)]
+    wts = inputs.make_weights(cfgs[0], "cuda")
+    ow = oracle.OracleWeights(wts, "bf16")
+    mbs = [inputs.make_microbatches(c, "cuda")[0] for c in cfgs]
+    refs = [oracle_run(cfgs[0], ow, mb) for mb in mbs]
+    # everything is allocated and copied before the first wait is enqueued:
+    # no later host-side copy may queue behind a wait on another stream
+    routing = [to_device_routing(mb.ids, mb.w) for mb in mbs]
+    recv = [_recv(cfgs[0]) for _ in mbs]
+    ready = [torch.zeros(D, dtype=torch.int32, device="cuda") for _ in mbs]
+    outs = [torch.full((T, cfgs[0].d), float("nan"), dtype=torch.bfloat16, device="cuda")
+            for _ in mbs]
+    s_late, s_rest = torch.cuda.Stream(), torch.cuda.Stream()
+    with ExpertStage(cfgs[0], wts, n_slots=3, max_tokens=T) as st:
+        ms = [st.microbatch(r[0], r[1], r[2], o) for r, o in zip(recv, outs)]
+        warm = torch.empty_like(outs[0])                  # first launches out of the way
+        st.submit(st.microbatch(mbs[0].x, routing[0][0], routing[0][1], warm), s_rest)
+        st.sync()
+        torch.cuda.synchronize()
+        log("late producer: A waits for senders not yet enqueued, B and C ready")
+        C.moe_ingest_wait(st.handle, ready[0], D, 1, 1 << 22, s_late)   # about 8 s at most
+        slot_a = st.submit(ms[0], s_late)
+        slots = []
+        for i in (1, 2):
+            _send(s_rest, mbs[i], recv[i], ready[i], 1, routing[i])
+            C.moe_ingest_wait(st.handle, ready[i], D, 1, 0, s_rest)
+            slots.append(st.submit(ms[i], s_rest))
+        assert len({slot_a, *slots}) == 3
+        t0 = time.time()
+        others_done = False
+        while time.time() - t0 < 4.0:
+            if all(C.moe_stage_poll(st.handle, s) == C.MOE_OK for s in slots):
+                others_done = True
+                break
+            time.sleep(0.001)
+        a_busy = C.moe_stage_poll(st.handle, slot_a) == C.MOE_EBUSY
+        log("  B, C done after %.1f ms: %s; A still busy: %s"
+            % ((time.time() - t0) * 1e3, others_done, a_busy))
+        _send(s_rest, mbs[0], recv[0], ready[0], 1, routing[0])  # A's senders, late
+        st.sync()
+        torch.cuda.synchronize()
+        assert C.moe_stage_poll(st.handle, slot_a) == C.MOE_OK
+    assert others_done, "B and C did not complete while A's senders were held back"
+    assert a_busy, "A completed before its senders were enqueued"
+    for i, name in enumerate("ABC"):
+        check_outputs(bf16_bits(outs[i]), refs[i], BF16_TOL, "micro-batch %s" % name)
