@@ -114,7 +114,9 @@ def run_workload(name, steps, warmup, n_buffers=3, repeats=5):
     stage = ExpertStage(cfg, w, n_slots=max(2, n_micro), max_tokens=max(Ts))
     mbs = [[stage.microbatch(x, i_, w_, o, xs) for (x, xs, i_, w_, o) in one] for one in sets]
     main = torch.cuda.Stream()
-    streams = [torch.cuda.Stream() for _ in range(n_micro)] if n_micro > 1 else [main]
+    # micro-batch 0 runs on the launch stream itself, the others on streams
+    # of their own: n_micro streams in all
+    streams = [main] + [torch.cuda.Stream() for _ in range(n_micro - 1)]
 
     def step(s):
         group = mbs[s % n_sets]
@@ -123,9 +125,15 @@ def run_workload(name, steps, warmup, n_buffers=3, repeats=5):
             return
         go = torch.cuda.Event()
         go.record(main)
-        for i, m in enumerate(group):
+        for i in range(1, n_micro):
             streams[i].wait_event(go)
+        for i, m in enumerate(group):
             stage.submit(m, streams[i])
+        # the join comes after every submission: the runtime maps streams
+        # onto a few hardware queues, and a wait enqueued on the launch
+        # stream between two submissions would hold back every later
+        # micro-batch whose stream shares that queue
+        for i in range(1, n_micro):
             done = torch.cuda.Event()
             done.record(streams[i])
             main.wait_event(done)
