@@ -63,6 +63,77 @@ __device__ __forceinline__ int lane_id() { return __lane_id(); }
 __device__ __forceinline__ bf16 f2bf(float v) { return static_cast<bf16>(v); }
 __device__ __forceinline__ float bf2f(bf16 v) { return static_cast<float>(v); }
 
+// Two fp32 values as a pair of bf16 in one word (round to nearest even), the
+// first in the low half.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
+{
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const bf16x2_t v = {static_cast<bf16>(lo), static_cast<bf16>(hi)};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// SiLU(g) * u = g / (1 + e^-g) * u with the hardware exp2 and reciprocal
+// (about 1 ulp each in fp32, far below the bf16 rounding of the result).
+// g -> -inf gives e = inf and a zero reciprocal; g -> +inf gives g * u.
+__device__ __forceinline__ float silu_mul(float g, float u)
+{
+    const float e = __builtin_amdgcn_exp2f(-1.44269504088896341f * g);
+    return g * __builtin_amdgcn_rcpf(1.0f + e) * u;
+}
+
+// Swaps lanes 32..63 of x with lanes 0..31 of y (v_permlane32_swap): after
+// it, x holds [x.lo, y.lo] and y holds [x.hi, y.hi].
+__device__ __forceinline__ void swap_halves(uint32_t &x, uint32_t &y)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(x, y, false, false);
+    x = r[0];
+    y = r[1];
+}
+
+// Output of one 32x32 block of the transposed product D[feature][token]
+// (v_mfma_f32_32x32x16_bf16 with the weights as its row operand): lane l
+// holds token l % 32, and register r holds feature 8 (r/4) + 4 (l/32) + r%4
+// of the block.  Lanes l and l ^ 32 hold the same token, so after swapping
+// halves each lane has 8 consecutive features and writes 16 bytes.
+//
+// store_block_bf16: the block's 32 features as bf16 at row[0..31] (row =
+// the token's output row at the block's first column); lane l writes
+// features 8 (l/32) .. +7 and 16 + 8 (l/32) .. +7.
+__device__ __forceinline__ void store_block_bf16(const f32x16 &v, bf16 *row, bool valid)
+{
+    uint32_t p[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        p[2 * q] = pack_bf16x2(v[4 * q], v[4 * q + 1]);
+        p[2 * q + 1] = pack_bf16x2(v[4 * q + 2], v[4 * q + 3]);
+    }
+    swap_halves(p[0], p[2]);
+    swap_halves(p[1], p[3]);
+    swap_halves(p[4], p[6]);
+    swap_halves(p[5], p[7]);
+    const int hi = (__lane_id() >> 5) * 8;
+    if (valid) {
+        *(u32x4 *)(row + hi) = (u32x4){p[0], p[1], p[2], p[3]};
+        *(u32x4 *)(row + 16 + hi) = (u32x4){p[4], p[5], p[6], p[7]};
+    }
+}
+
+// store_block_swiglu: the packed gate/up weights interleave by 16, so
+// features 0..15 of a block are gate rows and 16..31 the matching up rows:
+// register r (r < 8) and r + 8 of a lane are gate and up of one h column
+// 8 (r/4) + 4 (l/32) + r%4.  The block's 16 h columns go to hrow[0..15];
+// lane l writes h columns 8 (l/32) .. +7.
+__device__ __forceinline__ void store_block_swiglu(const f32x16 &v, bf16 *hrow, bool valid)
+{
+    uint32_t p[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        p[q] = pack_bf16x2(silu_mul(v[2 * q], v[2 * q + 8]), silu_mul(v[2 * q + 1], v[2 * q + 9]));
+    swap_halves(p[0], p[2]);
+    swap_halves(p[1], p[3]);
+    if (valid) *(u32x4 *)(hrow + (__lane_id() >> 5) * 8) = (u32x4){p[0], p[1], p[2], p[3]};
+}
+
 // e4m3 (OCP E4M3FN) code of v, round to nearest even.  |v| is clamped to 448
 // first, which makes the conversion saturating.
 __device__ __forceinline__ uint32_t e4m3_pack4(float a, float b, float c, float d)

@@ -46,10 +46,13 @@
 //    XCDs, so consecutive tile numbers are handed to the 32 workgroups of one
 //    XCD, and within a group (full) tiles are rastered in bands of 4 row-tiles,
 //    letting one XCD's L2 serve 4 row panels x 8 weight panels at a time;
+//  * the product is formed transposed (weights as the MFMA's row operand),
+//    so a lane's accumulators belong to one token and the output leaves as
+//    16-byte stores of 8 consecutive features (store_block_bf16);
 //  * SwiGLU mode fuses h = SiLU(gate) * up into the epilogue: the weight
-//    matrix packs gate and up rows in interleaved blocks of 16, so every
-//    32-column MFMA block holds matching gate and up columns, paired across
-//    lanes l and l ^ 16;
+//    matrix packs gate and up rows in interleaved blocks of 16, so a lane's
+//    registers r and r + 8 of a 32-column block are gate and up of the same
+//    h column (store_block_swiglu);
 //  * for the gate/up product, groups of at most kSmallRows rows are left to
 //    the small-group kernel (large_all = 0).
 #include "kernels.h"
@@ -173,7 +176,7 @@ __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const S
             for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
                 for (int nb = 0; nb < 2; ++nb)
-                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb],
+                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[nb], af[mb],
                                                                          acc[mb][nb], 0, 0, 0);
         };
         bf16x8 a0[NMB], b0[2], a1[NMB], b1[2];
@@ -210,36 +213,24 @@ __device__ __forceinline__ void run_tile(const Tile &t, const WaveConst &w, cons
     }
     __syncthreads();   // drain the look-ahead fills before the ring is reused
     if constexpr (NMB > 0) {
+        // transposed product: lane l holds token 32 mb + l % 32 of the wave's
+        // 128-row half (see store_block_bf16)
         bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb)
+        for (int mb = 0; mb < NMB; ++mb) {
+            const int tok = wm * 128 + mb * 32 + (lane & 31);
+            const bool valid = tok < rows_valid;
 #pragma unroll
             for (int nb = 0; nb < 2; ++nb) {
-                const f32x16 v = acc[mb][nb];
-                const int rbase = wm * 128 + mb * 32 + w.rd_hi * 4;
-                if constexpr (SWIGLU) {
-                    const int f = N / 2;
-                    const bool gl = (lane & 16) == 0;
-                    const int hc = (n0 + wn * 64 + nb * 32) / 2 + (lane & 15);
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const float up = __shfl_xor(v[r], 16);
-                        const int lr = rbase + (r >> 2) * 8 + (r & 3);
-                        if (gl && lr < rows_valid)
-                            C[(int64_t)(row0 + lr) * f + hc] =
-                                f2bf(v[r] / (1.0f + __expf(-v[r])) * up);
-                    }
-                } else {
-                    const int col = n0 + wn * 64 + nb * 32 + (lane & 31);
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int lr = rbase + (r >> 2) * 8 + (r & 3);
-                        if (lr < rows_valid && col < N)
-                            C[(int64_t)(row0 + lr) * N + col] = f2bf(v[r]);
-                    }
-                }
-                __builtin_amdgcn_sched_barrier(0);
+                const int col = n0 + wn * 64 + nb * 32;
+                if constexpr (SWIGLU)
+                    store_block_swiglu(acc[mb][nb], C + (int64_t)(row0 + tok) * (N / 2) + col / 2,
+                                       valid);
+                else
+                    store_block_bf16(acc[mb][nb], C + (int64_t)(row0 + tok) * N + col,
+                                     valid && col < N);
             }
+        }
     }
 }
 

@@ -21,9 +21,16 @@
 //    constant, and every step issues the same loads (steps past K re-read
 //    the last one), so the wait at each step is a constant: the loads of
 //    the two steps issued after it;
-//  * SwiGLU: packed gate/up columns interleave by 16, so each 32-column
-//    block is 16 gate and 16 up columns of the same h columns, paired
-//    across lanes l and l ^ 16.
+//  * the product is formed transposed (weights as the MFMA's row operand),
+//    so each lane ends with one token's accumulators: with gate/up columns
+//    interleaved by 16, a lane's registers r and r + 8 are gate and up of
+//    the same h column, and h leaves as 16-byte stores (store_block_swiglu);
+//  * the epilogue is shared by the four waves: wave (kh, ch) hands its
+//    partial sums of column block 1 - kh to its K-half partner through LDS
+//    and finishes column block kh of every row block;
+//  * the group tables are read in one round trip (a ballot over st_base
+//    finds a tile's group), so the first fills are not held back by a chain
+//    of dependent loads.
 #include "kernels.h"
 
 namespace moe {
@@ -135,29 +142,75 @@ __device__ __forceinline__ void small_step(const SmallTile &t, const SmallLds &l
     for (int mb = 0; mb < NMB; ++mb)
         a1[mb] = *(const bf16x8 *)&As[(mb * 32 + rd_row) * kRowEs + (((c0 + 2) ^ swz) << 3)];
     __builtin_amdgcn_sched_barrier(0);
+    // transposed product: the weights are the MFMA's row operand, so a lane's
+    // accumulators belong to one token (see store_block_bf16)
 #pragma unroll
     for (int mb = 0; mb < NMB; ++mb) {
-        acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[mb], breg[I][0], acc[mb][0], 0, 0, 0);
-        acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[mb], breg[I][2], acc[mb][1], 0, 0, 0);
+        acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(breg[I][0], a0[mb], acc[mb][0], 0, 0, 0);
+        acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(breg[I][2], a0[mb], acc[mb][1], 0, 0, 0);
     }
 #pragma unroll
     for (int mb = 0; mb < NMB; ++mb) {
-        acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mb], breg[I][1], acc[mb][0], 0, 0, 0);
-        acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mb], breg[I][3], acc[mb][1], 0, 0, 0);
+        acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(breg[I][1], a1[mb], acc[mb][0], 0, 0, 0);
+        acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(breg[I][3], a1[mb], acc[mb][1], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// One tile with NMB 32-row blocks: K loop, K-half reduction and epilogue,
-// fully unrolled over the row blocks so no accumulator crosses a branch.
 // K-half partials of column half ch: block q = 2 mb + cb (16 x 64 floats,
-// 4 KB) lives in ring buffer 2 ch + q / 6 at 4 KB (q % 6).  Callers pass q
-// from fully unrolled loops, so it folds to a base plus an immediate.
-__device__ __forceinline__ float *partial_block(const SmallLds &l, int ch, int q)
+// 4 KB, register group g of lane l at float4 64 g + l) lives in ring buffer
+// 2 ch + q / 6 at 4 KB (q % 6).  Callers pass q from fully unrolled loops, so
+// it folds to a base plus an immediate.
+__device__ __forceinline__ f32x4 *partial_block(const SmallLds &l, int ch, int q)
 {
-    return (float *)(ch ? l.a[2 + q / 6] : l.a[q / 6]) + (q % 6) * 16 * 64;
+    return (f32x4 *)((ch ? l.a[2 + q / 6] : l.a[q / 6]) + (q % 6) * 2048);
 }
 
+// K-half exchange, step 1: wave (kh, ch) finishes column block kh of every
+// row block, so it hands its partial sums of column block 1 - kh (CB = kh)
+// to wave (1 - kh, ch).
+template <int NMB, int CB>
+__device__ __forceinline__ void give_partials(const SmallLds &l, const SmallWave &w,
+                                              const f32x16 (&acc)[NMB][2])
+{
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+        f32x4 *part = partial_block(l, w.ch, 2 * mb + 1 - CB) + w.lane;
+        const f32x16 &v = acc[mb][1 - CB];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            part[g * 64] = (f32x4){v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]};
+    }
+}
+
+// Step 2: add the partner's partial sums of column block CB and write the
+// block: h = SiLU(gate) * up (16 h columns) or the product (32 columns).
+template <bool SWIGLU, int NMB, int CB>
+__device__ __forceinline__ void finish_blocks(const SmallTile &t, const SmallLds &l,
+                                              const SmallWave &w, const f32x16 (&acc)[NMB][2])
+{
+    const int col = t.n0 + w.ch * 64 + CB * 32;      // first weight column of the block
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+        f32x16 v = acc[mb][CB];
+        const f32x4 *part = partial_block(l, w.ch, 2 * mb + CB) + w.lane;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const f32x4 p = part[g * 64];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[4 * g + e] += p[e];
+        }
+        const int tok = mb * 32 + (w.lane & 31);
+        const bool valid = tok < t.rows_valid;
+        if constexpr (SWIGLU)
+            store_block_swiglu(v, t.C + (int64_t)(t.row0 + tok) * (t.N / 2) + col / 2, valid);
+        else
+            store_block_bf16(v, t.C + (int64_t)(t.row0 + tok) * t.N + col, valid && col < t.N);
+    }
+}
+
+// One tile with NMB 32-row blocks: K loop, K-half reduction and epilogue,
+// fully unrolled over the row blocks so no accumulator crosses a branch.
 template <bool SWIGLU, int NMB>
 __device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLds &l,
                                                const SmallWave &w)
@@ -188,55 +241,12 @@ __device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLd
     // partials overwrite next: wait for every load of this wave, then sync.
     __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0)
     __syncthreads();   // all ring reads done: the ring now holds the K-half partials
-
-    // wave (1, ch) hands its partial sums to wave (0, ch), lane-contiguous
-    if (w.kh == 1) {
-#pragma unroll
-        for (int mb = 0; mb < NMB; ++mb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                float *part = partial_block(l, w.ch, mb * 2 + cb) + w.lane;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) part[r * 64] = acc[mb][cb][r];
-            }
-    }
+    // Every wave writes half the blocks: the VALU work of the epilogue (fp32
+    // sums, SiLU, bf16 packing) is shared by all four.
+    if (w.kh == 0) give_partials<NMB, 0>(l, w, acc); else give_partials<NMB, 1>(l, w, acc);
     __syncthreads();
-    if (w.kh == 0) {
-        // Epilogue, one 32x32 block at a time: register r of a block = row
-        // 8 (r/4) + 4 (lane/32) + r%4, column lane % 32 of the block.
-        const int rd_hi = w.lane >> 5;
-#pragma unroll
-        for (int mb = 0; mb < NMB; ++mb)
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                f32x16 v = acc[mb][cb];
-                const float *part = partial_block(l, w.ch, mb * 2 + cb) + w.lane;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) v[r] += part[r * 64];
-                const int cbase = t.n0 + w.ch * 64 + cb * 32;
-                if constexpr (SWIGLU) {
-                    const int f = t.N / 2;
-                    const bool gl = (w.lane & 16) == 0;
-                    const int hc = cbase / 2 + (w.lane & 15);
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const float up = __shfl_xor(v[r], 16);
-                        const int lr = mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
-                        if (gl && lr < t.rows_valid)
-                            t.C[(int64_t)(t.row0 + lr) * f + hc] =
-                                f2bf(v[r] / (1.0f + __expf(-v[r])) * up);
-                    }
-                } else {
-                    const int col = cbase + (w.lane & 31);
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int lr = mb * 32 + (r >> 2) * 8 + rd_hi * 4 + (r & 3);
-                        if (lr < t.rows_valid && col < t.N)
-                            t.C[(int64_t)(t.row0 + lr) * t.N + col] = f2bf(v[r]);
-                    }
-                }
-            }
-    }
+    if (w.kh == 0) finish_blocks<SWIGLU, NMB, 0>(t, l, w, acc);
+    else finish_blocks<SWIGLU, NMB, 1>(t, l, w, acc);
     __syncthreads();   // partials read before the next tile's fills reuse the ring
 }
 
@@ -261,7 +271,20 @@ void k_gemm_bf16_small(GemmArgs a)
     w.ch = w.wave & 1;
     const int N = a.N, K = a.K;
     const int NT = (N + kTNs - 1) / kTNs;
-    const int total = __builtin_amdgcn_readfirstlane(a.groups.st_base[a.G] * NT);
+    // The group tables in one round trip: with G < 64 groups, lane i holds
+    // st_base[i] (i <= G), rows[i] and row0[i] (i < G), and a tile's group is
+    // found by a ballot instead of a chain of dependent loads.
+    const int G = a.G;
+    const bool few = G < 64;
+    int st_l = 0, rows_l = 0, row0_l = 0;
+    if (few) {
+        const int gi = min(w.lane, G - 1);
+        st_l = a.groups.st_base[min(w.lane, G)];
+        rows_l = a.groups.rows[gi];
+        row0_l = a.groups.row0[gi];
+    }
+    const int total = __builtin_amdgcn_readfirstlane(
+        (few ? __builtin_amdgcn_readlane(st_l, G) : a.groups.st_base[G]) * NT);
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
     if (first >= total) return;      // no tile: leave before resolving the weights
@@ -279,15 +302,24 @@ void k_gemm_bf16_small(GemmArgs a)
         // blocks are consecutive, so one XCD shares its token rows in L2)
         const int j = L / NT;
         const int nt = L - j * NT;
-        int lo = 0, hi = a.G;                    // largest g with st_base[g] <= j
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (a.groups.st_base[mid] <= j) lo = mid; else hi = mid;
-        }
         SmallTile t;
-        const int g = __builtin_amdgcn_readfirstlane(lo);
-        t.rows_valid = __builtin_amdgcn_readfirstlane(a.groups.rows[g]);
-        t.row0 = __builtin_amdgcn_readfirstlane(a.groups.row0[g]);
+        int g;                                   // largest g < G with st_base[g] <= j
+        if (few) {
+            // st_base is nondecreasing with st_base[0] = 0 <= j
+            g = __builtin_popcountll(__ballot(w.lane < G && st_l <= j)) - 1;
+            g = __builtin_amdgcn_readfirstlane(g);
+            t.rows_valid = __builtin_amdgcn_readlane(rows_l, g);
+            t.row0 = __builtin_amdgcn_readlane(row0_l, g);
+        } else {
+            int lo = 0, hi = G;
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (a.groups.st_base[mid] <= j) lo = mid; else hi = mid;
+            }
+            g = __builtin_amdgcn_readfirstlane(lo);
+            t.rows_valid = __builtin_amdgcn_readfirstlane(a.groups.rows[g]);
+            t.row0 = __builtin_amdgcn_readfirstlane(a.groups.row0[g]);
+        }
         t.n0 = nt * kTNs;
         t.N = N;
         t.K = K;
