@@ -28,6 +28,10 @@ constexpr uint32_t kDefaultIngestSpins = 1u << 19;   // about a second of pollin
 constexpr int kBM = 256;
 constexpr int kBN = 256;
 
+// Cache-policy operand of the raw buffer loads: non-temporal (streaming)
+// data, read once, evicted first and kept out of the last-level cache.
+constexpr int kNonTemporal = 2;
+
 // Sticky error bits.
 constexpr int kErrBadId = 1;
 constexpr int kErrBadLayer = 2;

@@ -126,7 +126,7 @@ struct Stage {
 // offset, which the buffer range check covers (rows past the group read as
 // zero); the scalar offset, which it does not cover, only moves along K and
 // between weight column blocks that exist (absent ones re-read the last).
-template <bool AROWS>
+template <bool AROWS, bool STREAM>
 __device__ __forceinline__ void fill(const Tile &t, const WaveConst &w, const Stage &st, int j)
 {
     const int js = min(j, t.KT - 1);
@@ -143,13 +143,13 @@ __device__ __forceinline__ void fill(const Tile &t, const WaveConst &w, const St
         const int cb = min(f >> 1, t.ncb - 1), kk = f & 1;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             t.rb, (lds_void *)(st.b + f * 512), 16, w.voff_b,
-            cb * w.cbstride + (js * 2 + kk) * 1024, 0, 0);
+            cb * w.cbstride + (js * 2 + kk) * 1024, 0, STREAM ? kNonTemporal : 0);
     }
 }
 
 // One K step: wait for this step's stage, sync, refill the stage freed by
 // the previous step, then 2 sub-steps of 8 MFMAs.
-template <int S, int NMB>
+template <int S, int NMB, bool STREAM>
 __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const Stage (&ring)[4],
                                       f32x16 (&acc)[NMB > 0 ? NMB : 1][2], int j)
 {
@@ -157,7 +157,7 @@ __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const S
     constexpr int kAfter = 2 * (NMB > 0 ? 4 : 2);
     __builtin_amdgcn_s_waitcnt((kAfter & 15) | ((kAfter >> 4) << 14) | (7 << 4) | (15 << 8));
     __builtin_amdgcn_s_barrier();   // every wave's fill of step j landed; step j-1 read
-    fill<(NMB > 0)>(t, w, ring[(S + 3) & 3], j + 3);
+    fill<(NMB > 0), STREAM>(t, w, ring[(S + 3) & 3], j + 3);
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (NMB > 0) {
         const bf16 *As = ring[S].a;
@@ -193,7 +193,7 @@ __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const S
 // K loop, then the epilogue.  NMB = 0 only for the upper half of a tile of
 // at most 128 rows: the wave then loads no token rows (they are all past the
 // group) and runs no MFMAs, but still fills its share of weight fragments.
-template <bool SWIGLU, int NMB>
+template <bool SWIGLU, int NMB, bool STREAM>
 __device__ __forceinline__ void run_tile(const Tile &t, const WaveConst &w, const Stage (&ring)[4],
                                          const GemmArgs &a, int N, int n0, int row0, int rows_valid,
                                          bool sh, int wm, int wn, int lane)
@@ -201,15 +201,15 @@ __device__ __forceinline__ void run_tile(const Tile &t, const WaveConst &w, cons
     f32x16 acc[NMB > 0 ? NMB : 1][2];
 #pragma unroll
     for (int i = 0; i < (NMB > 0 ? NMB : 1); ++i) acc[i][0] = acc[i][1] = (f32x16){};
-    fill<(NMB > 0)>(t, w, ring[0], 0);
-    fill<(NMB > 0)>(t, w, ring[1], 1);
-    fill<(NMB > 0)>(t, w, ring[2], 2);
+    fill<(NMB > 0), STREAM>(t, w, ring[0], 0);
+    fill<(NMB > 0), STREAM>(t, w, ring[1], 1);
+    fill<(NMB > 0), STREAM>(t, w, ring[2], 2);
     // K is a multiple of 128, so KT is a multiple of 4.
     for (int j = 0; j < t.KT; j += 4) {
-        kstep<0, NMB>(t, w, ring, acc, j);
-        kstep<1, NMB>(t, w, ring, acc, j + 1);
-        kstep<2, NMB>(t, w, ring, acc, j + 2);
-        kstep<3, NMB>(t, w, ring, acc, j + 3);
+        kstep<0, NMB, STREAM>(t, w, ring, acc, j);
+        kstep<1, NMB, STREAM>(t, w, ring, acc, j + 1);
+        kstep<2, NMB, STREAM>(t, w, ring, acc, j + 2);
+        kstep<3, NMB, STREAM>(t, w, ring, acc, j + 3);
     }
     __syncthreads();   // drain the look-ahead fills before the ring is reused
     if constexpr (NMB > 0) {
@@ -336,12 +336,27 @@ void k_gemm_bf16(GemmArgs a)
         const int nmb = by_size ? __builtin_amdgcn_readfirstlane(
                                       min(4, max(0, (rows_valid - wm * 128 + 31) >> 5)))
                                 : 4;
-        switch (nmb) {
-        case 0: run_tile<SWIGLU, 0>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
-        case 1: run_tile<SWIGLU, 1>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
-        case 2: run_tile<SWIGLU, 2>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
-        case 3: run_tile<SWIGLU, 3>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
-        default: run_tile<SWIGLU, 4>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+        // A group of one row tile reads each of its weight panels once in the
+        // launch: those loads are non-temporal, so the panels do not displace
+        // what the caches hold for later kernels (the combine's rows) and the
+        // dirty lines of earlier ones.  Groups of several row tiles share
+        // their panels through L2 and keep ordinary loads.
+        if (grows <= kBM) {
+            switch (nmb) {
+            case 0: run_tile<SWIGLU, 0, true>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            case 1: run_tile<SWIGLU, 1, true>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            case 2: run_tile<SWIGLU, 2, true>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            case 3: run_tile<SWIGLU, 3, true>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            default: run_tile<SWIGLU, 4, true>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            }
+        } else {
+            switch (nmb) {
+            case 0: run_tile<SWIGLU, 0, false>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            case 1: run_tile<SWIGLU, 1, false>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            case 2: run_tile<SWIGLU, 2, false>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            case 3: run_tile<SWIGLU, 3, false>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            default: run_tile<SWIGLU, 4, false>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
+            }
         }
     }
 }

@@ -14,7 +14,10 @@
 //    once per tile;
 //  * weights go straight from HBM into a 4-deep register ring (each wave
 //    loads only its own columns and K half: four 1 KB fragments per step,
-//    each a contiguous load thanks to the fragment-order weight layout), so
+//    each a contiguous load thanks to the fragment-order weight layout);
+//    they are read once, so the loads are non-temporal and the stream does
+//    not displace the activations other kernels read next, nor force out
+//    the dirty lines of earlier ones while it runs; so
 //    LDS carries only the token rows: a direct-to-LDS 4-deep ring
 //    (4 x 24 KB) read as MFMA fragments, two per row block per step;
 //  * the K loop is unrolled by 4 so every ring index is a compile-time
@@ -67,7 +70,8 @@ __device__ __forceinline__ int token_row_offset(const int32_t *index, int div, i
 
 __device__ __forceinline__ bf16x8 load_b128(__amdgpu_buffer_rsrc_t r, int voff, int soff)
 {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    // every weight byte is read once in the launch: non-temporal
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kNonTemporal);
     return __builtin_bit_cast(bf16x8, v);
 }
 
@@ -221,9 +225,16 @@ __device__ __forceinline__ void run_small_tile(const SmallTile &t, const SmallLd
     for (int i = 0; i < NMB; ++i) acc[i][0] = acc[i][1] = (f32x16){};
     bf16x8 breg[kRing][4];
 
+    // Each step's loads stay together and in step order, as in the loop: the
+    // compiler's wait for a weight register at the loop's first step then
+    // matches the loop's own (interleaved prologue loads made it wait for
+    // the next step's loads at every fourth step).
     fill_step<NMB, 0>(t, l, w, 0, breg);
+    __builtin_amdgcn_sched_barrier(0);
     fill_step<NMB, 1>(t, l, w, 1, breg);
+    __builtin_amdgcn_sched_barrier(0);
     fill_step<NMB, 2>(t, l, w, 2, breg);
+    __builtin_amdgcn_sched_barrier(0);
     // K is a multiple of 128, so KT is even: groups of 4 steps, then 2.
     int k = 0;
     for (; k + 4 <= t.KT; k += 4) {
