@@ -33,20 +33,22 @@
 //    stay in flight) and no wait drains the look-ahead;
 //  * the weights are packed in the 16 x 128 fragment order of the MFMA (two
 //    lane-contiguous 1 KB halves per fragment), gate and up rows interleaved
-//    by 64, so each wave's 64 features lie in one 128 x 128 scale block (one
-//    scalar weight scale per wave and group) and a 256-feature gate/up tile
-//    covers exactly one 128-channel group of h;
+//    by 16, so each wave's 64 features are gate and up rows of the same 32 h
+//    channels (one scalar scale each per group: the gate and the up 128 x 128
+//    block) and a 256-feature gate/up tile covers exactly one 128-channel
+//    group of h;
 //  * token rows are 128-byte rows whose 16-byte chunks are XOR-swizzled by
 //    (row / 2) % 8; rows past a group's end have an offset past every buffer
 //    range and read as zero; the scalar offset, which the range check does
 //    not cover, only moves along K (clamped to the last group) and between
 //    weight fragments that exist;
-//  * SwiGLU mode: the up waves hand their accumulators to the gate waves
-//    through LDS, the gate waves form h = SiLU(gate) * up in fp32 and
-//    quantise each token's 128 channels to e4m3 with one fp32 scale (the same
-//    arithmetic as the activation quantiser), and the tile's 128 rows of 128
-//    codes are written out through LDS as 16-byte stores.  The down product
-//    writes bf16, four consecutive features per lane.
+//  * SwiGLU mode: every wave forms h = SiLU(gate) * up in fp32 for its 32
+//    channels, the per-token |h| maximum over the tile's 128 channels meets
+//    in a 2 KB LDS table, and each token's channels are quantised to e4m3
+//    with one fp32 scale amax / 448 (the activation quantiser's scale;
+//    the quotient is taken as a product with the scale's reciprocal), four
+//    codes per lane and store.  The down product writes bf16, four
+//    consecutive features per lane.
 #include "kernels.h"
 
 namespace moe {
@@ -81,7 +83,8 @@ struct Tile8 {
     __amdgpu_buffer_rsrc_t rw, rx, rs;
     int vx[2];          // token fills: rows 16 w + 8 i + lane / 8, swizzled chunk (or past the range)
     int KT, ncb, cbstride, s_ld;
-    const cfloat *sbp;  // this wave's weight scale of each K group
+    const cfloat *sbp0; // weight scale of each K group: feature blocks rb = 0, 2 of this wave
+    const cfloat *sbp1; //   ... and rb = 1, 3 (in SwiGLU mode the up rows; otherwise = sbp0)
 };
 
 struct Ring8 {
@@ -128,7 +131,7 @@ struct Wave8 {
 // group (wave-uniform); the weight scale of the next group is loaded ahead.
 template <int S, int NCB>
 __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ring8 (&ring)[3],
-                                        f32x4 (&acc)[4][4], float &sb_next, int kg)
+                                        f32x4 (&acc)[4][4], float (&sb_next)[2], int kg)
 {
     // The loads issued after this group's fills are the next group's seven.
     // lgkmcnt(0): this wave's reads of the previous group's stage have
@@ -136,8 +139,9 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
     // the scheduler lets that group's MFMAs run past this point.
     __builtin_amdgcn_s_waitcnt((kFillLoads & 15) | ((kFillLoads >> 4) << 14) | (7 << 4) | (0 << 8));
     __builtin_amdgcn_s_barrier();   // every wave's fills of group kg landed; group kg-1 read
-    const float sb = sb_next;
-    sb_next = t.sbp[min(kg + 1, t.KT - 1)];
+    const float sb0 = sb_next[0], sb1 = sb_next[1];
+    sb_next[0] = t.sbp0[min(kg + 1, t.KT - 1)];
+    sb_next[1] = t.sbp1[min(kg + 1, t.KT - 1)];
     __builtin_amdgcn_sched_barrier(0);
     fill8(t, ring[(S + 2) % 3], w.wave, w.lane, kg + 2);
     __builtin_amdgcn_sched_barrier(0);
@@ -173,10 +177,10 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
                         wfr[rb], xf[cb], (f32x4){}, 0, 0, 0, 127, 0, 127);
             }
             if (cb > 0) {
-                const float s = st[cb - 1] * sb;
+                const float s0 = st[cb - 1] * sb0, s1 = st[cb - 1] * sb1;
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb)
-                    acc[rb][cb - 1] = tq[(cb - 1) & 1][rb] * s + acc[rb][cb - 1];
+                    acc[rb][cb - 1] = tq[(cb - 1) & 1][rb] * ((rb & 1) ? s1 : s0) + acc[rb][cb - 1];
             }
         }
     }
@@ -187,7 +191,7 @@ template <int NCB>
 __device__ __forceinline__ void kloop8(const Tile8 &t, const Wave8 &w, const Ring8 (&ring)[3],
                                        f32x4 (&acc)[4][4])
 {
-    float sb_next = t.sbp[0];
+    float sb_next[2] = {t.sbp0[0], t.sbp1[0]};
     __builtin_amdgcn_sched_barrier(0);
     fill8(t, ring[0], w.wave, w.lane, 0);
     fill8(t, ring[1], w.wave, w.lane, 1);
@@ -221,8 +225,7 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
     __shared__ __attribute__((aligned(1024))) uint8_t lds_x1[kXSBytes];
     __shared__ __attribute__((aligned(1024))) uint8_t lds_x2[kXSBytes];
     __shared__ int32_t ttab[kMaxLocalExperts + 2];    // prefix of 128-token tiles per group
-    float *const lds_s0 = (float *)(lds_x0 + kXBytes);
-    float *const lds_s1 = (float *)(lds_x1 + kXBytes);
+    __shared__ float hmax[4][kTokT];                   // SwiGLU: |h| maximum per wave and token
     const Ring8 ring[3] = {{lds_w0, lds_x0, (float *)(lds_x0 + kXBytes)},
                            {lds_w1, lds_x1, (float *)(lds_x1 + kXBytes)},
                            {lds_w2, lds_x2, (float *)(lds_x2 + kXBytes)}};
@@ -317,17 +320,19 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
             const int r = frow + 8 * i;
             t.vx[i] = r < rows_valid ? r * K + fch[i] : (int)0x80000000u;
         }
-        const float *sbp;
+        const float *sbp0, *sbp1;
         if constexpr (SWIGLU) {
             // [G][f/128][gate, up][K/128]: tile nt covers gate/up scale block nt
             const int f = N / 2;
-            sbp = Bsw + (((int64_t)g * (f / 128) + nt) * 2 + (w.wf & 1)) * t.KT;
+            sbp0 = Bsw + ((int64_t)g * (f / 128) + nt) * 2 * t.KT;
+            sbp1 = sbp0 + t.KT;
         } else {
             // [G][N/128][K/128]: wave features n0 + 64 wf .. + 63
             const int nb = min(2 * nt + (w.wf >> 1), N / 128 - 1);
-            sbp = Bsw + ((int64_t)g * (N / 128) + nb) * t.KT;
+            sbp0 = sbp1 = Bsw + ((int64_t)g * (N / 128) + nb) * t.KT;
         }
-        t.sbp = (const cfloat *)(uintptr_t)sbp;
+        t.sbp0 = (const cfloat *)(uintptr_t)sbp0;
+        t.sbp1 = (const cfloat *)(uintptr_t)sbp1;
 
         f32x4 acc[4][4];
 #pragma unroll
@@ -353,69 +358,49 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
         const int tok = w.wt * 64 + (lane & 15);        // + 16 cb
         const int fq = 4 * (lane >> 4);                 // + 16 rb + i
         if constexpr (SWIGLU) {
+            // Gate and up rows interleave by 16: blocks rb = 2 p and 2 p + 1 are
+            // gate and up of h channels 32 wf + 16 p + 4 (lane / 16) + i of the
+            // tile's 128, so every wave forms its own h.  A token's scale needs
+            // |h| over all 128 channels: each wave reduces its 32 (lanes
+            // l, l ^ 16, l ^ 32, l ^ 48 hold the same token), and the four
+            // waves of the same tokens meet in LDS.
             const int f = N / 2;
-            const int s_ld = t.s_ld;
+            f32x4 h[2][4];
+            float am[4];
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                float m = 0.0f;
+#pragma unroll
+                for (int pq = 0; pq < 2; ++pq)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float hv = silu_mul(acc[2 * pq][cb][i], acc[2 * pq + 1][cb][i]);
+                        h[pq][cb][i] = hv;
+                        m = fmaxf(m, fabsf(hv));
+                    }
+                m = fmaxf(m, __shfl_xor(m, 16));
+                am[cb] = fmaxf(m, __shfl_xor(m, 32));
+                if (lane < 16) hmax[w.wf][tok + 16 * cb] = am[cb];
+            }
+            __syncthreads();
             uint8_t *H = (uint8_t *)(sh ? a.C_shared : a.C_routed);
-            float *Hs = (sh ? a.Cs_shared : a.Cs_routed) + (int64_t)nt * s_ld + row0;
-            // wave pair: gate wf = 2 q, up wf = 2 q + 1, same tokens; h
-            // channels 64 q .. 64 q + 63 of the tile's 128
-            const int q = w.wf >> 1;
-            const int p = q + 2 * w.wt;
-            float *xch = (float *)((p < 2 ? lds_w0 : lds_w1) + (p & 1) * (kWBytes / 2));
-            if (w.wf & 1) {
+            float *Hs = (sh ? a.Cs_shared : a.Cs_routed) + (int64_t)nt * t.s_ld + row0;
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb)
+            for (int cb = 0; cb < 4; ++cb) {
+                const int tk = tok + 16 * cb;
+                const float amax = fmaxf(fmaxf(hmax[0][tk], hmax[1][tk]), fmaxf(hmax[2][tk], hmax[3][tk]));
+                const float sc = amax > 0.0f ? amax / 448.0f : 1.0f;   // the activation quantiser's scale
+                const float inv = __builtin_amdgcn_rcpf(sc);
+                if (tk < rows_valid) {
+                    uint8_t *dst = H + (int64_t)(row0 + tk) * f + nt * 128 + w.wf * 32 + fq;
 #pragma unroll
-                    for (int cb = 0; cb < 4; ++cb)
-                        *(f32x4 *)&xch[((rb * 4 + cb) * 64 + lane) * 4] = acc[rb][cb];
-            }
-            __syncthreads();
-            float *mx = q ? lds_s1 : lds_s0;          // per token: max |h| over this wave's 64 channels
-            if (!(w.wf & 1)) {
-#pragma unroll
-                for (int cb = 0; cb < 4; ++cb) {
-                    float am = 0.0f;
-#pragma unroll
-                    for (int rb = 0; rb < 4; ++rb) {
-                        const f32x4 up = *(const f32x4 *)&xch[((rb * 4 + cb) * 64 + lane) * 4];
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float gt = acc[rb][cb][i];
-                            const float hv = gt / (1.0f + __expf(-gt)) * up[i];
-                            acc[rb][cb][i] = hv;
-                            am = fmaxf(am, fabsf(hv));
-                        }
-                    }
-                    am = fmaxf(am, __shfl_xor(am, 16));
-                    am = fmaxf(am, __shfl_xor(am, 32));
-                    if (lane < 16) mx[tok + 16 * cb] = am;
+                    for (int pq = 0; pq < 2; ++pq)
+                        *(uint32_t *)(dst + 16 * pq) =
+                            e4m3_pack4(h[pq][cb][0] * inv, h[pq][cb][1] * inv,
+                                       h[pq][cb][2] * inv, h[pq][cb][3] * inv);
+                    if (w.wf == 0 && lane < 16) Hs[tk] = sc;
                 }
             }
-            __syncthreads();
-            uint8_t *stg = lds_x2;   // [128 tokens][128 codes]
-            if (!(w.wf & 1)) {
-#pragma unroll
-                for (int cb = 0; cb < 4; ++cb) {
-                    const int tk = tok + 16 * cb;
-                    const float am = fmaxf(lds_s0[tk], lds_s1[tk]);
-                    const float s = am > 0.0f ? am / 448.0f : 1.0f;   // IEEE division
-#pragma unroll
-                    for (int rb = 0; rb < 4; ++rb) {
-                        const uint32_t c4 = e4m3_pack4(acc[rb][cb][0] / s, acc[rb][cb][1] / s,
-                                                       acc[rb][cb][2] / s, acc[rb][cb][3] / s);
-                        *(uint32_t *)&stg[tk * kGrpB + q * 64 + rb * 16 + fq] = c4;
-                    }
-                    if (q == 0 && lane < 16 && tk < rows_valid) Hs[tk] = s;
-                }
-            }
-            __syncthreads();
-            for (int c = tid; c < kTokT * (kGrpB / 16); c += kThreads8) {
-                const int row = c >> 3, ch = c & 7;
-                if (row < rows_valid)
-                    *(uint4 *)&H[(int64_t)(row0 + row) * f + nt * 128 + ch * 16] =
-                        *(const uint4 *)&stg[row * kGrpB + ch * 16];
-            }
-            __syncthreads();   // the staging areas are the next tile's first stages
         } else {
             bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
             const int fb = n0 + w.wf * 64 + fq;

@@ -167,11 +167,12 @@ hipError_t launch_ingest_signal(uint32_t *word, uint32_t epoch, hipStream_t s);
 
 // Weight packing at create time.  Gate and up rows are interleaved in
 // blocks of `interleave` rows: packed row 2*il*b + i is gate row il*b + i for
-// i < il and up row il*b + (i - il) otherwise.  bf16 uses il = 16 (a 32-column
-// MFMA block then holds matching gate and up columns); fp8 uses il = 64 (each
-// wave's 64 columns are all gate or all up rows of one 128-row scale block).
+// i < il and up row il*b + (i - il) otherwise.  Both paths use il = 16: a
+// 32-column bf16 MFMA block then holds matching gate and up columns, and in
+// fp8 a wave's 64 columns are gate and up rows of the same 32 h channels,
+// all within one 128-row scale block of each.
 constexpr int kInterleaveBf16 = 16;
-constexpr int kInterleaveFp8 = 64;
+constexpr int kInterleaveFp8 = 16;
 // bf16 weights in MFMA fragment order (the layout both bf16 grouped-GEMM
 // kernels read B in): chunk ((m * N/32 + n/32) * K/16 + k/16) * 64 + n % 32 +
 // 32 ((k/8) % 2) of 16 bytes holds row n, columns k..k+7 (k % 8 == 0).  With

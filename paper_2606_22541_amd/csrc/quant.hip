@@ -59,7 +59,7 @@ hipError_t launch_quantize_fp8(const void *x, int32_t n_rows, const int32_t *n_r
 // ---------------------------------------------------------------------------
 // Gate/up weight scales of the fp8 path: [m][f/128][gate, up][d/128], so
 // that a 256-column tile of the packed matrix (gate and up rows
-// [128 t, 128 t + 128), interleaved by 64) finds both of its scale rows
+// [128 t, 128 t + 128), interleaved by 16) finds both of its scale rows
 // next to each other.
 __global__ void k_pack_gate_up_scales(const float *__restrict__ gs, const float *__restrict__ us,
                                       float *__restrict__ ps, int32_t n_mats, int32_t f,

@@ -218,7 +218,7 @@ moe_status record(SlotWs &sl, hipStream_t s)
 
 // Packs one layer's weights into w1/w2 (and fp8 scales into s1/s2) in MFMA
 // fragment order; the shared expert is group E_loc.  [gate|up] is
-// interleaved by 16 rows (bf16) or 64 rows (fp8).
+// interleaved by 16 rows.
 hipError_t pack_layer(const moe_stage_desc *d, const Sizes &z, const moe_weights *w, void *w1,
                       void *w2, float *s1, float *s2, hipStream_t s)
 {
