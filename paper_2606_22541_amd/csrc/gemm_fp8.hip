@@ -168,6 +168,7 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
             st[cb] = Ss[w.s_rd + cb * 16];
         }
         f32x4 tq[2][4];
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int cb = 0; cb <= NCB; ++cb) {
             if (cb < NCB) {
@@ -183,6 +184,20 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
                     acc[rb][cb - 1] = tq[(cb - 1) & 1][rb] * ((rb & 1) ? s1 : s0) + acc[rb][cb - 1];
             }
         }
+        // Issue order: the first token block's four MFMAs, then one MFMA per
+        // four promotion instructions (an MFMA holds the matrix core for 32
+        // cycles, in which the wave's VALU port is free for independent
+        // work), then the last block's promotion.  The scheduler's own order
+        // ran the MFMAs and the promotion in separate bursts.
+#pragma unroll
+        for (int i = 0; i < 4; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+#pragma unroll
+        for (int i = 0; i < 4 * (NCB - 1); ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                            // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);                            // VALU
+        }
+        __builtin_amdgcn_sched_group_barrier(0x002, 32, 0);
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
