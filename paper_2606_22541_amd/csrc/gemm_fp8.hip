@@ -129,9 +129,13 @@ struct Wave8 {
 // previous group used with group kg + 2, then the 16 MFMAs with the
 // promotion of each token block.  NCB token blocks of 16 hold tokens of the
 // group (wave-uniform); the weight scale of the next group is loaded ahead.
+// The last token block's products are promoted at the start of the next
+// group (pend, with their scales ps), while that group's LDS reads are in
+// flight, instead of after the group's last MFMAs.
 template <int S, int NCB>
 __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ring8 (&ring)[3],
-                                        f32x4 (&acc)[4][4], float (&sb_next)[2], int kg)
+                                        f32x4 (&acc)[4][4], float (&sb_next)[2], int kg,
+                                        f32x4 (&pend)[4], float (&ps)[2])
 {
     // The loads issued after this group's fills are the next group's seven.
     // lgkmcnt(0): this wave's reads of the previous group's stage have
@@ -167,15 +171,19 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
             xf[cb] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
             st[cb] = Ss[w.s_rd + cb * 16];
         }
+        // the previous group's last token block, complete long since
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+            acc[rb][NCB - 1] = pend[rb] * ps[rb & 1] + acc[rb][NCB - 1];
         f32x4 tq[2][4];
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int cb = 0; cb <= NCB; ++cb) {
-            if (cb < NCB) {
+        for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb)
-                    tq[cb & 1][rb] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
-                        wfr[rb], xf[cb], (f32x4){}, 0, 0, 0, 127, 0, 127);
+            for (int rb = 0; rb < 4; ++rb) {
+                const f32x4 p = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
+                    wfr[rb], xf[cb], (f32x4){}, 0, 0, 0, 127, 0, 127);
+                if (cb == NCB - 1) pend[rb] = p; else tq[cb & 1][rb] = p;
             }
             if (cb > 0) {
                 const float s0 = st[cb - 1] * sb0, s1 = st[cb - 1] * sb1;
@@ -184,11 +192,13 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
                     acc[rb][cb - 1] = tq[(cb - 1) & 1][rb] * ((rb & 1) ? s1 : s0) + acc[rb][cb - 1];
             }
         }
+        ps[0] = st[NCB - 1] * sb0;
+        ps[1] = st[NCB - 1] * sb1;
         // Issue order: the first token block's four MFMAs, then one MFMA per
         // four promotion instructions (an MFMA holds the matrix core for 32
         // cycles, in which the wave's VALU port is free for independent
-        // work), then the last block's promotion.  The scheduler's own order
-        // ran the MFMAs and the promotion in separate bursts.
+        // work).  The scheduler's own order ran the MFMAs and the promotion
+        // in separate bursts.
 #pragma unroll
         for (int i = 0; i < 4; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
 #pragma unroll
@@ -196,7 +206,7 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                            // MFMA
             __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);                            // VALU
         }
-        __builtin_amdgcn_sched_group_barrier(0x002, 32, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
         __builtin_amdgcn_sched_barrier(0);
     }
 }
@@ -207,6 +217,8 @@ __device__ __forceinline__ void kloop8(const Tile8 &t, const Wave8 &w, const Rin
                                        f32x4 (&acc)[4][4])
 {
     float sb_next[2] = {t.sbp0[0], t.sbp1[0]};
+    f32x4 pend[4] = {};
+    float ps[2] = {0.0f, 0.0f};
     __builtin_amdgcn_sched_barrier(0);
     fill8(t, ring[0], w.wave, w.lane, 0);
     fill8(t, ring[1], w.wave, w.lane, 1);
@@ -214,12 +226,17 @@ __device__ __forceinline__ void kloop8(const Tile8 &t, const Wave8 &w, const Rin
     // remaining one or two groups
     int kg = 0;
     for (; kg + 3 <= t.KT; kg += 3) {
-        kgroup8<0, NCB>(t, w, ring, acc, sb_next, kg);
-        kgroup8<1, NCB>(t, w, ring, acc, sb_next, kg + 1);
-        kgroup8<2, NCB>(t, w, ring, acc, sb_next, kg + 2);
+        kgroup8<0, NCB>(t, w, ring, acc, sb_next, kg, pend, ps);
+        kgroup8<1, NCB>(t, w, ring, acc, sb_next, kg + 1, pend, ps);
+        kgroup8<2, NCB>(t, w, ring, acc, sb_next, kg + 2, pend, ps);
     }
-    if (kg < t.KT) kgroup8<0, NCB>(t, w, ring, acc, sb_next, kg);
-    if (kg + 1 < t.KT) kgroup8<1, NCB>(t, w, ring, acc, sb_next, kg + 1);
+    if (kg < t.KT) kgroup8<0, NCB>(t, w, ring, acc, sb_next, kg, pend, ps);
+    if (kg + 1 < t.KT) kgroup8<1, NCB>(t, w, ring, acc, sb_next, kg + 1, pend, ps);
+    if constexpr (NCB > 0) {
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+            acc[rb][NCB - 1] = pend[rb] * ps[rb & 1] + acc[rb][NCB - 1];
+    }
 }
 
 }  // namespace
