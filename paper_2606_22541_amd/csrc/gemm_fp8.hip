@@ -21,16 +21,20 @@
 //    weights are the MFMA's row operand and the tokens its column operand,
 //    so each lane holds four consecutive features of ONE token and the
 //    token's fp32 scale is a single value per lane and 16-token block;
-//  * eight wave64s (two per SIMD, so one wave's promotion arithmetic runs
-//    beside the other's MFMAs), wave w owning features 64 (w % 4) .. + 63
-//    and tokens 64 (w / 4) .. + 63 of the tile as 4 x 4 blocks of
-//    v_mfma_scale_f32_16x16x128_f8f6f4;
+//  * eight wave64s, wave w owning features 64 (w % 4) .. + 63 and tokens
+//    64 (w / 4) .. + 63 of the tile as 4 x 4 blocks of
+//    v_mfma_scale_f32_16x16x128_f8f6f4; the two waves of a SIMD (w and
+//    w + 4) work in opposite phases, one reading its operands from LDS
+//    while the other runs its MFMAs and promotion (the K loop below);
 //  * K advances one scale group (128 bytes) per step through a 3-deep LDS
 //    ring of 48.5 KB stages (32 KB of weight fragments, 16 KB of token rows,
 //    the step's 128 token scales) filled by direct-to-LDS buffer loads two
 //    groups ahead: every group issues the same seven loads per wave, so the
 //    wait before a group is the constant vmcnt(7) (the next group's fills
-//    stay in flight) and no wait drains the look-ahead;
+//    stay in flight) and no wait drains the look-ahead.  The loads go out
+//    one by one between the MFMAs: a stage is 49 loads of 1 KB per CU, about
+//    as many clocks of the per-CU load path as the group's MFMAs take, and
+//    issued as one burst they held back every wave's instructions;
 //  * the weights are packed in the 16 x 128 fragment order of the MFMA (two
 //    lane-contiguous 1 KB halves per fragment), gate and up rows interleaved
 //    by 16, so each wave's 64 features are gate and up rows of the same 32 h
@@ -99,23 +103,31 @@ struct Ring8 {
 //    (l % 8) ^ ((row / 2) % 8);
 //  * 64 of the 128 token scales (waves w and w + 2, w + 4, w + 6 load the
 //    same ones: identical data to identical addresses).
-__device__ __forceinline__ void fill8(const Tile8 &t, const Ring8 &st, int wave, int lane, int kg)
+// Load i (0..6) of the fills: 0..3 the weight fragment halves, 4..5 the
+// token rows, 6 the token scales.
+__device__ __forceinline__ void fill8_one(const Tile8 &t, const Ring8 &st, int wave, int lane, int kg,
+                                          int i)
 {
     const int ks = min(kg, t.KT - 1);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    if (i < 4) {
         const int f = wave * 2 + (i >> 1), h = i & 1;
         const int cb = min(f, t.ncb - 1);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(t.rw, (lds_void *)(st.w + f * 2048 + h * 1024), 16,
                                                  lane * 16, cb * t.cbstride + ks * 2048 + h * 1024,
                                                  0, 0);
+    } else if (i < 6) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(t.rx, (lds_void *)(st.x + (wave * 16 + (i - 4) * 8) * kGrpB),
+                                                 16, t.vx[i - 4], ks * kGrpB, 0, 0);
+    } else {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(t.rs, (lds_void *)(st.s + (wave & 1) * 64), 4,
+                                                 (ks * t.s_ld + (wave & 1) * 64 + lane) * 4, 0, 0, 0);
     }
+}
+
+__device__ __forceinline__ void fill8(const Tile8 &t, const Ring8 &st, int wave, int lane, int kg)
+{
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(t.rx, (lds_void *)(st.x + (wave * 16 + i * 8) * kGrpB),
-                                                 16, t.vx[i], ks * kGrpB, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(t.rs, (lds_void *)(st.s + (wave & 1) * 64), 4,
-                                             (ks * t.s_ld + (wave & 1) * 64 + lane) * 4, 0, 0, 0);
+    for (int i = 0; i < kFillLoads; ++i) fill8_one(t, st, wave, lane, kg, i);
 }
 
 struct Wave8 {
@@ -125,39 +137,35 @@ struct Wave8 {
     int s_rd;           // LDS float index of this lane's token scale (token block 0)
 };
 
-// One K group on stage S: wait for its fills, sync, refill the stage the
-// previous group used with group kg + 2, then the 16 MFMAs with the
-// promotion of each token block.  NCB token blocks of 16 hold tokens of the
-// group (wave-uniform); the weight scale of the next group is loaded ahead.
-// The last token block's products are promoted at the start of the next
-// group (pend, with their scales ps), while that group's LDS reads are in
-// flight, instead of after the group's last MFMAs.
+// The K loop runs two waves per SIMD in opposite phases ("ping-pong"):
+// waves 0..3 (tokens 0..63 of the tile) read group g's operands from LDS
+// while waves 4..7 (tokens 64..127) run group g-1's MFMAs, and at the next
+// barrier the roles swap, so one wave's LDS reads run under the other's
+// matrix-core work instead of every wave reading, then every wave
+// multiplying.  In slots E_g, O_g (one barrier before each):
+//
+//   slot   waves 0..3          waves 4..7
+//   E_g    read g              MFMAs of g-1
+//   O_g    MFMAs of g          read g
+//
+// Every wave issues its fills of group g+2 at the start of E_g, into the
+// stage of group g-1, which waves 0..3 read in E_{g-1} (and consumed in
+// O_{g-1}) and waves 4..7 in O_{g-1} (and waited for before E_g).  Before
+// the barrier that starts E_g each wave waits for its own fills of g; only
+// those of g+1 (seven loads) stay in flight.
+
+// LDS reads of group g from stage S into registers: the four weight
+// fragments, the NCB token fragments and their token scales.  The previous
+// group's last token block is promoted here, under the reads' latency.
 template <int S, int NCB>
-__device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ring8 (&ring)[3],
-                                        f32x4 (&acc)[4][4], float (&sb_next)[2], int kg,
-                                        f32x4 (&pend)[4], float (&ps)[2])
+__device__ __forceinline__ void read8(const Wave8 &w, const Ring8 (&ring)[3], i32x8 (&wfr)[4],
+                                      i32x8 (&xf)[4], float (&st)[4], f32x4 (&acc)[4][4],
+                                      const f32x4 (&pend)[4], const float (&ps)[2])
 {
-    // The loads issued after this group's fills are the next group's seven.
-    // lgkmcnt(0): this wave's reads of the previous group's stage have
-    // returned, so after the barrier that stage may be refilled even where
-    // the scheduler lets that group's MFMAs run past this point.
-    __builtin_amdgcn_s_waitcnt((kFillLoads & 15) | ((kFillLoads >> 4) << 14) | (7 << 4) | (0 << 8));
-    __builtin_amdgcn_s_barrier();   // every wave's fills of group kg landed; group kg-1 read
-    const float sb0 = sb_next[0], sb1 = sb_next[1];
-    sb_next[0] = t.sbp0[min(kg + 1, t.KT - 1)];
-    sb_next[1] = t.sbp1[min(kg + 1, t.KT - 1)];
-    __builtin_amdgcn_sched_barrier(0);
-    fill8(t, ring[(S + 2) % 3], w.wave, w.lane, kg + 2);
-    __builtin_amdgcn_sched_barrier(0);
     if constexpr (NCB > 0) {
         const uint8_t *Ws = ring[S].w;
         const uint8_t *Xs = ring[S].x;
         const float *Ss = ring[S].s;
-        // every operand of the group first (one LDS latency per group), then
-        // the MFMAs of token block cb interleaved with the promotion of block
-        // cb - 1, whose products are complete by then
-        i32x8 wfr[4], xf[NCB];
-        float st[NCB];
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
             const i32x4 lo = *(const i32x4 *)&Ws[w.w_rd + rb * 2048];
@@ -171,19 +179,42 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
             xf[cb] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
             st[cb] = Ss[w.s_rd + cb * 16];
         }
-        // the previous group's last token block, complete long since
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb)
             acc[rb][NCB - 1] = pend[rb] * ps[rb & 1] + acc[rb][NCB - 1];
+    }
+}
+
+// The 4 x NCB MFMAs of one group, each token block's products promoted
+// (acc += t * s_X * s_W) while the next block's MFMAs run; the last block's
+// products are left in pend with their scales in ps.  The wave's seven fill
+// loads of group kgf go out two per token block, after its second and fourth
+// MFMA (the rest after the last MFMA when NCB < 4): the per-CU load path
+// accepts about one 1 KB load every 19 clocks, and fills issued as one burst
+// by every wave hold each wave's later instructions until the load path has
+// taken them.
+template <int NCB, bool FILL = true>
+__device__ __forceinline__ void mfma8(const i32x8 (&wfr)[4], const i32x8 (&xf)[4],
+                                      const float (&st)[4], float sb0, float sb1,
+                                      f32x4 (&acc)[4][4], f32x4 (&pend)[4], float (&ps)[2],
+                                      const Tile8 &t, const Ring8 &fst, int wave, int lane, int kgf)
+{
+    constexpr int kInter = !FILL ? 0 : (2 * NCB < kFillLoads) ? 2 * NCB : kFillLoads;
+    if constexpr (NCB > 0) {
         f32x4 tq[2][4];
-        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
+            // one token block: its four MFMAs with two fill loads, and the
+            // previous block's promotion, in a fixed issue order (one MFMA,
+            // then four promotion instructions, while the MFMA holds the
+            // matrix core for 32 cycles)
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb) {
                 const f32x4 p = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
                     wfr[rb], xf[cb], (f32x4){}, 0, 0, 0, 127, 0, 127);
                 if (cb == NCB - 1) pend[rb] = p; else tq[cb & 1][rb] = p;
+                const int j = 2 * cb + (rb >> 1);
+                if ((rb & 1) && j < kInter) fill8_one(t, fst, wave, lane, kgf, j);
             }
             if (cb > 0) {
                 const float s0 = st[cb - 1] * sb0, s1 = st[cb - 1] * sb1;
@@ -191,47 +222,104 @@ __device__ __forceinline__ void kgroup8(const Tile8 &t, const Wave8 &w, const Ri
                 for (int rb = 0; rb < 4; ++rb)
                     acc[rb][cb - 1] = tq[(cb - 1) & 1][rb] * ((rb & 1) ? s1 : s0) + acc[rb][cb - 1];
             }
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
+                if (cb > 0) __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);           // VALU
+                if ((rb & 1) && 2 * cb + (rb >> 1) < kInter)
+                    __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);                    // VMEM
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
         ps[0] = st[NCB - 1] * sb0;
         ps[1] = st[NCB - 1] * sb1;
-        // Issue order: the first token block's four MFMAs, then one MFMA per
-        // four promotion instructions (an MFMA holds the matrix core for 32
-        // cycles, in which the wave's VALU port is free for independent
-        // work).  The scheduler's own order ran the MFMAs and the promotion
-        // in separate bursts.
+    }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-#pragma unroll
-        for (int i = 0; i < 4 * (NCB - 1); ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                            // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);                            // VALU
-        }
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    for (int i = kInter; i < (FILL ? kFillLoads : 0); ++i) fill8_one(t, fst, wave, lane, kgf, i);
+}
+
+// s_waitcnt operands (gfx9 encoding: vmcnt [3:0] and [15:14], expcnt [6:4],
+// lgkmcnt [11:8]).
+constexpr int kWaitFills = (kFillLoads & 15) | ((kFillLoads >> 4) << 14) | (7 << 4) | (15 << 8);
+constexpr int kWaitLds = 15 | (3 << 14) | (7 << 4) | (0 << 8);
+
+// A slot boundary, with the wait before it: the scheduler moves nothing
+// across it (a wait drawn into the slot before it would shorten the
+// fills' look-ahead).
+template <int WAIT>
+__device__ __forceinline__ void slot_barrier()
+{
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (WAIT >= 0) __builtin_amdgcn_s_waitcnt(WAIT);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Group g (stage S) for a wave of either half.  LEAD: waves 0..3.  MFMA_PREV:
+// the trailing half has a group g-1 to multiply (g > 0).
+template <int S, int NCB, bool LEAD, bool MFMA_PREV>
+__device__ __forceinline__ void group8(const Tile8 &t, const Wave8 &w, const Ring8 (&ring)[3],
+                                       f32x4 (&acc)[4][4], i32x8 (&wfr)[4], i32x8 (&xf)[4],
+                                       float (&st)[4], float (&sb)[2], float (&sb_next)[2],
+                                       f32x4 (&pend)[4], float (&ps)[2], int kg)
+{
+    slot_barrier<kWaitFills>();                   // E_kg, after this wave's fills of group kg
+    const Ring8 &fst = ring[(S + 2) % 3];         // group kg+2's stage, read last by group kg-1
+    if constexpr (LEAD) {
+        sb[0] = sb_next[0];
+        sb[1] = sb_next[1];
+        sb_next[0] = t.sbp0[min(kg + 1, t.KT - 1)];
+        sb_next[1] = t.sbp1[min(kg + 1, t.KT - 1)];
+        read8<S, NCB>(w, ring, wfr, xf, st, acc, pend, ps);
+        slot_barrier<-1>();                       // O_kg
+        mfma8<NCB>(wfr, xf, st, sb[0], sb[1], acc, pend, ps, t, fst, w.wave, w.lane, kg + 2);
+    } else {
+        if constexpr (MFMA_PREV)
+            mfma8<NCB>(wfr, xf, st, sb[0], sb[1], acc, pend, ps, t, fst, w.wave, w.lane, kg + 2);
+        else
+            fill8(t, fst, w.wave, w.lane, kg + 2);
+        slot_barrier<-1>();                       // O_kg
+        sb[0] = sb_next[0];
+        sb[1] = sb_next[1];
+        sb_next[0] = t.sbp0[min(kg + 1, t.KT - 1)];
+        sb_next[1] = t.sbp1[min(kg + 1, t.KT - 1)];
+        read8<S, NCB>(w, ring, wfr, xf, st, acc, pend, ps);
+        // the reads of stage S complete before E_{kg+1}, where it is refilled
         __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(kWaitLds);
     }
 }
 
-// The K loop of one tile for a wave with NCB token blocks holding tokens.
-template <int NCB>
+// The K loop of one tile for a wave of one half with NCB token blocks
+// holding tokens.  Both halves pass 2 KT + 1 barriers.
+template <bool LEAD, int NCB>
 __device__ __forceinline__ void kloop8(const Tile8 &t, const Wave8 &w, const Ring8 (&ring)[3],
                                        f32x4 (&acc)[4][4])
 {
+    float sb[2] = {0.0f, 0.0f};
     float sb_next[2] = {t.sbp0[0], t.sbp1[0]};
     f32x4 pend[4] = {};
     float ps[2] = {0.0f, 0.0f};
+    i32x8 wfr[4], xf[4];
+    float st[4];
     __builtin_amdgcn_sched_barrier(0);
     fill8(t, ring[0], w.wave, w.lane, 0);
     fill8(t, ring[1], w.wave, w.lane, 1);
-    // a branch-free body of three groups (stage = group % 3), then the
-    // remaining one or two groups
-    int kg = 0;
+    // the first group (the trailing half has nothing to multiply yet), a
+    // branch-free body of three groups (stage = group % 3), then the rest
+    group8<0, NCB, LEAD, false>(t, w, ring, acc, wfr, xf, st, sb, sb_next, pend, ps, 0);
+    int kg = 1;
     for (; kg + 3 <= t.KT; kg += 3) {
-        kgroup8<0, NCB>(t, w, ring, acc, sb_next, kg, pend, ps);
-        kgroup8<1, NCB>(t, w, ring, acc, sb_next, kg + 1, pend, ps);
-        kgroup8<2, NCB>(t, w, ring, acc, sb_next, kg + 2, pend, ps);
+        group8<1, NCB, LEAD, true>(t, w, ring, acc, wfr, xf, st, sb, sb_next, pend, ps, kg);
+        group8<2, NCB, LEAD, true>(t, w, ring, acc, wfr, xf, st, sb, sb_next, pend, ps, kg + 1);
+        group8<0, NCB, LEAD, true>(t, w, ring, acc, wfr, xf, st, sb, sb_next, pend, ps, kg + 2);
     }
-    if (kg < t.KT) kgroup8<0, NCB>(t, w, ring, acc, sb_next, kg, pend, ps);
-    if (kg + 1 < t.KT) kgroup8<1, NCB>(t, w, ring, acc, sb_next, kg + 1, pend, ps);
+    if (kg < t.KT) group8<1, NCB, LEAD, true>(t, w, ring, acc, wfr, xf, st, sb, sb_next, pend, ps, kg);
+    if (kg + 1 < t.KT) group8<2, NCB, LEAD, true>(t, w, ring, acc, wfr, xf, st, sb, sb_next, pend, ps, kg + 1);
+    // E_KT: the trailing half multiplies the last group
+    slot_barrier<-1>();
+    if constexpr (!LEAD)
+        mfma8<NCB, false>(wfr, xf, st, sb[0], sb[1], acc, pend, ps, t, ring[0], w.wave, w.lane, 0);
     if constexpr (NCB > 0) {
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb)
@@ -375,12 +463,22 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
         // 16-token blocks of this wave's 64 tokens that hold tokens of the group
         const int ncbw = __builtin_amdgcn_readfirstlane(
             min(4, max(0, rows_valid - w.wt * 64 + 15) / 16));
-        switch (ncbw) {
-        case 0: kloop8<0>(t, w, ring, acc); break;
-        case 1: kloop8<1>(t, w, ring, acc); break;
-        case 2: kloop8<2>(t, w, ring, acc); break;
-        case 3: kloop8<3>(t, w, ring, acc); break;
-        default: kloop8<4>(t, w, ring, acc); break;
+        if (w.wt == 0) {
+            switch (ncbw) {
+            case 0: kloop8<true, 0>(t, w, ring, acc); break;
+            case 1: kloop8<true, 1>(t, w, ring, acc); break;
+            case 2: kloop8<true, 2>(t, w, ring, acc); break;
+            case 3: kloop8<true, 3>(t, w, ring, acc); break;
+            default: kloop8<true, 4>(t, w, ring, acc); break;
+            }
+        } else {
+            switch (ncbw) {
+            case 0: kloop8<false, 0>(t, w, ring, acc); break;
+            case 1: kloop8<false, 1>(t, w, ring, acc); break;
+            case 2: kloop8<false, 2>(t, w, ring, acc); break;
+            case 3: kloop8<false, 3>(t, w, ring, acc); break;
+            default: kloop8<false, 4>(t, w, ring, acc); break;
+            }
         }
         __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0): the clamped look-ahead fills
         __syncthreads();                                     // ring idle in every wave
