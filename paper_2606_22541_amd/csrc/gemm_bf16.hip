@@ -18,7 +18,9 @@
 //    vector L1 and its data return path, which then limits the MFMA rate);
 //    K advances 32 bf16 per step through a 4-deep ring of 32 KB stages
 //    (16 KB of token rows, 16 KB of weight fragments) filled by
-//    direct-to-LDS buffer loads three steps ahead;
+//    direct-to-LDS buffer loads three steps ahead, issued one at a time
+//    between the MFMAs (the per-CU load path takes a 1 KB load about every
+//    19 clocks, and a burst of every wave's loads stalled the waves behind it);
 //  * token rows are 64 bytes per step in LDS, their 16-byte chunks
 //    XOR-swizzled by (row / 4) % 4 so that the 16-lane groups of each
 //    ds_read_b128 hit 64 distinct banks; weight fragments arrive in MFMA
@@ -126,20 +128,17 @@ struct Stage {
 // offset, which the buffer range check covers (rows past the group read as
 // zero); the scalar offset, which it does not cover, only moves along K and
 // between weight column blocks that exist (absent ones re-read the last).
-template <bool AROWS, bool STREAM>
-__device__ __forceinline__ void fill(const Tile &t, const WaveConst &w, const Stage &st, int j)
+// Load i of a fill: 0, 1 the token rows, 2, 3 the weight fragments.
+template <bool STREAM>
+__device__ __forceinline__ void fill_one(const Tile &t, const WaveConst &w, const Stage &st, int j, int i)
 {
     const int js = min(j, t.KT - 1);
-    if constexpr (AROWS) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                t.ra, (lds_void *)(st.a + (w.wave * 32 + i * 16) * kRowElems), 16,
-                i ? t.va1 : t.va0, js * kBK * 2, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int f = w.wave * 2 + i;             // fragment of the stage: 2 cb + kk
+    if (i < 2) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            t.ra, (lds_void *)(st.a + (w.wave * 32 + i * 16) * kRowElems), 16,
+            i ? t.va1 : t.va0, js * kBK * 2, 0, 0);
+    } else {
+        const int f = w.wave * 2 + (i - 2);       // fragment of the stage: 2 cb + kk
         const int cb = min(f >> 1, t.ncb - 1), kk = f & 1;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             t.rb, (lds_void *)(st.b + f * 512), 16, w.voff_b,
@@ -147,8 +146,16 @@ __device__ __forceinline__ void fill(const Tile &t, const WaveConst &w, const St
     }
 }
 
-// One K step: wait for this step's stage, sync, refill the stage freed by
-// the previous step, then 2 sub-steps of 8 MFMAs.
+template <bool AROWS, bool STREAM>
+__device__ __forceinline__ void fill(const Tile &t, const WaveConst &w, const Stage &st, int j)
+{
+#pragma unroll
+    for (int i = AROWS ? 0 : 2; i < 4; ++i) fill_one<STREAM>(t, w, st, j, i);
+}
+
+// One K step: wait for this step's stage, sync, then 2 sub-steps of 2 NMB
+// MFMAs with the refill of the stage freed by the previous step (step j+3)
+// spread among them.
 template <int S, int NMB, bool STREAM>
 __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const Stage (&ring)[4],
                                       f32x16 (&acc)[NMB > 0 ? NMB : 1][2], int j)
@@ -157,8 +164,8 @@ __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const S
     constexpr int kAfter = 2 * (NMB > 0 ? 4 : 2);
     __builtin_amdgcn_s_waitcnt((kAfter & 15) | ((kAfter >> 4) << 14) | (7 << 4) | (15 << 8));
     __builtin_amdgcn_s_barrier();   // every wave's fill of step j landed; step j-1 read
-    fill<(NMB > 0), STREAM>(t, w, ring[(S + 3) & 3], j + 3);
     __builtin_amdgcn_sched_barrier(0);
+    if constexpr (NMB == 0) fill<false, STREAM>(t, w, ring[(S + 3) & 3], j + 3);
     if constexpr (NMB > 0) {
         const bf16 *As = ring[S].a;
         const bf16 *Bs = ring[S].b;
@@ -183,8 +190,23 @@ __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const S
         read(0, a0, b0);
         read(1, a1, b1);
         __builtin_amdgcn_sched_barrier(0);
-        mma(a0, b0);
-        mma(a1, b1);
+        // the fills of step j+3 go out between the MFMAs, one per NMB MFMAs:
+        // issued as one burst after the barrier (32 loads of 1 KB per CU),
+        // they held back every wave's reads and MFMAs until the per-CU load
+        // path had taken them
+        constexpr int kM = 4 * NMB, kEvery = kM / 4;
+        int nf = 0;
+#pragma unroll
+        for (int q = 0; q < kM; ++q) {
+            const int kk = q / (2 * NMB), r = q % (2 * NMB), mb = r >> 1, nb = r & 1;
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kk ? b1[nb] : b0[nb], kk ? a1[mb] : a0[mb],
+                                                                 acc[mb][nb], 0, 0, 0);
+            if (q % kEvery == kEvery / 2 && nf < 4) {
+                fill_one<STREAM>(t, w, ring[(S + 3) & 3], j + 3, nf);
+                ++nf;
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
         __builtin_amdgcn_sched_barrier(0);
     }
 }
