@@ -119,6 +119,34 @@ __device__ __forceinline__ void fill_step(const SmallTile &t, const SmallLds &l,
     breg[I][3] = load_b128(t.rb, w.vb + w.cbstride + 1024, soff);
 }
 
+// Inside the K loop the same loads are split: the step's four weight loads
+// first (the HBM stream), then one token-row load after each row block's
+// first two MFMAs, so that the per-CU load path is not handed the whole
+// step's loads at once while the MFMAs wait behind them.  Each step still
+// issues exactly NMB + 4 loads, all after the previous step's, so the waits
+// keep their counts.
+template <int I>
+__device__ __forceinline__ void fill_weights(const SmallTile &t, const SmallWave &w, int j,
+                                             bf16x8 (&breg)[kRing][4])
+{
+    const int js = min(j, t.KT - 1);
+    const int soff = js * 4 * 1024;
+    breg[I][0] = load_b128(t.rb, w.vb, soff);
+    breg[I][1] = load_b128(t.rb, w.vb + 1024, soff);
+    breg[I][2] = load_b128(t.rb, w.vb + w.cbstride, soff);
+    breg[I][3] = load_b128(t.rb, w.vb + w.cbstride + 1024, soff);
+}
+
+template <int I>
+__device__ __forceinline__ void fill_row(const SmallTile &t, const SmallLds &l, const SmallWave &w,
+                                         int j, int i)
+{
+    const int js = min(j, t.KT - 1);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        t.ra, (lds_void_s *)(l.a[I] + (w.wave + 4 * i) * 8 * kRowEs), 16, t.avoff[i],
+        js * kBKs * 2, 0, 0);
+}
+
 // One K step with compile-time ring index I = k % 4.
 template <int NMB, int I>
 __device__ __forceinline__ void small_step(const SmallTile &t, const SmallLds &l,
@@ -129,7 +157,7 @@ __device__ __forceinline__ void small_step(const SmallTile &t, const SmallLds &l
     constexpr int kAfter = 2 * (NMB + 4);
     __builtin_amdgcn_s_waitcnt((kAfter & 15) | ((kAfter >> 4) << 14) | (7 << 4) | (15 << 8));
     __builtin_amdgcn_s_barrier();          // every wave's fills of step k landed; step k-1 read
-    fill_step<NMB, (I + 3) & 3>(t, l, w, k + 3, breg);
+    fill_weights<(I + 3) & 3>(t, w, k + 3, breg);
     __builtin_amdgcn_sched_barrier(0);
 
     // Token-row fragment (mb, m) of sub-step kk = 2 kh + m: row
@@ -152,6 +180,8 @@ __device__ __forceinline__ void small_step(const SmallTile &t, const SmallLds &l
     for (int mb = 0; mb < NMB; ++mb) {
         acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(breg[I][0], a0[mb], acc[mb][0], 0, 0, 0);
         acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(breg[I][2], a0[mb], acc[mb][1], 0, 0, 0);
+        fill_row<(I + 3) & 3>(t, l, w, k + 3, mb);
+        __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int mb = 0; mb < NMB; ++mb) {
