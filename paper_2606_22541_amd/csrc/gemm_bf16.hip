@@ -12,7 +12,11 @@
 //    re-launch) and empty experts simply own no tiles;
 //  * a 256x256 output tile per workgroup, eight wave64s (two per SIMD, so one
 //    wave's MFMAs cover the other's waits) each owning a 128x64 block as 4x2
-//    blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation);
+//    blocks of v_mfma_f32_32x32x16_bf16 (fp32 accumulation); in a full tile
+//    the two waves of a SIMD (the tile's two 128-row halves) run the K loop
+//    in opposite phases, one reading its operands from LDS while the other
+//    multiplies (in a partial tile the halves have unequal work, which the
+//    alternation would serialise, so all waves read, then multiply);
 //  * both operands are staged once per workgroup in LDS (staging the weights
 //    per wave instead would load every weight fragment twice through the
 //    vector L1 and its data return path, which then limits the MFMA rate);
@@ -211,6 +215,128 @@ __device__ __forceinline__ void kstep(const Tile &t, const WaveConst &w, const S
     }
 }
 
+// Full tiles (256 rows: both halves hold four row blocks) run the K loop
+// with the two waves of a SIMD (w and w + 4: the tile's two 128-row halves)
+// in opposite phases.  In phase E of step j waves 0..3 read
+// step j's operands from LDS while waves 4..7 run step j-1's MFMAs, and in
+// phase O the roles swap; a workgroup barrier separates the phases.  Every
+// wave's fills of step j+3 go out between its MFMAs (waves 4..7 in phase E,
+// waves 0..3 in phase O), into the stage of step j-1, which both halves have
+// read by then; before the barrier that opens phase E of step j each wave
+// waits for its own fills of step j.
+
+template <int S, int NMB>
+__device__ __forceinline__ void read_step(const WaveConst &w, const Stage (&ring)[4],
+                                          bf16x8 (&a0)[4], bf16x8 (&a1)[4], bf16x8 (&b0)[2],
+                                          bf16x8 (&b1)[2])
+{
+    if constexpr (NMB > 0) {
+        const bf16 *As = ring[S].a;
+        const bf16 *Bs = ring[S].b;
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            const int ch = ((kk * 2 + w.rd_hi) ^ w.swz) << 3;
+#pragma unroll
+            for (int mb = 0; mb < NMB; ++mb)
+                (kk ? a1 : a0)[mb] = *(const bf16x8 *)&As[w.a_rd + mb * 32 * kRowElems + ch];
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb)
+                (kk ? b1 : b0)[nb] = *(const bf16x8 *)&Bs[w.b_rd + (nb * 2 + kk) * 512];
+        }
+    }
+}
+
+// The 4 NMB MFMAs of one step, with this wave's fills of step jf spread
+// among them (one per NMB MFMAs) when FILL; a wave without row blocks only
+// fills its weight fragments.
+template <int NMB, bool STREAM, bool FILL>
+__device__ __forceinline__ void mma_step(const Tile &t, const WaveConst &w, const Stage &fst, int jf,
+                                         f32x16 (&acc)[NMB > 0 ? NMB : 1][2], const bf16x8 (&a0)[4],
+                                         const bf16x8 (&a1)[4], const bf16x8 (&b0)[2],
+                                         const bf16x8 (&b1)[2])
+{
+    if constexpr (NMB == 0) {
+        if constexpr (FILL) fill<false, STREAM>(t, w, fst, jf);
+    } else {
+        constexpr int kM = 4 * NMB, kEvery = kM / 4;
+        int nf = 0;
+#pragma unroll
+        for (int q = 0; q < kM; ++q) {
+            const int kk = q / (2 * NMB), r = q % (2 * NMB), mb = r >> 1, nb = r & 1;
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kk ? b1[nb] : b0[nb], kk ? a1[mb] : a0[mb],
+                                                                 acc[mb][nb], 0, 0, 0);
+            if (FILL && q % kEvery == kEvery / 2 && nf < 4) {
+                fill_one<STREAM>(t, w, fst, jf, nf);
+                ++nf;
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void phase_barrier()
+{
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Step j on stage S for a wave of either half.  LEAD: waves 0..3.  PREV: the
+// trailing half has a step j-1 to multiply (j > 0).
+template <int S, int NMB, bool STREAM, bool LEAD, bool PREV>
+__device__ __forceinline__ void pp_step(const Tile &t, const WaveConst &w, const Stage (&ring)[4],
+                                        f32x16 (&acc)[NMB > 0 ? NMB : 1][2], bf16x8 (&a0)[4],
+                                        bf16x8 (&a1)[4], bf16x8 (&b0)[2], bf16x8 (&b1)[2], int j)
+{
+    // the fills of steps j+1 and j+2 are the loads issued after step j's
+    constexpr int kAfter = 2 * (NMB > 0 ? 4 : 2);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt((kAfter & 15) | ((kAfter >> 4) << 14) | (7 << 4) | (15 << 8));
+    phase_barrier();                                        // E_j
+    const Stage &fst = ring[(S + 3) & 3];
+    if constexpr (LEAD) {
+        read_step<S, NMB>(w, ring, a0, a1, b0, b1);
+        phase_barrier();                                    // O_j
+        mma_step<NMB, STREAM, true>(t, w, fst, j + 3, acc, a0, a1, b0, b1);
+    } else {
+        if constexpr (PREV) mma_step<NMB, STREAM, true>(t, w, fst, j + 3, acc, a0, a1, b0, b1);
+        else fill<(NMB > 0), STREAM>(t, w, fst, j + 3);
+        phase_barrier();                                    // O_j
+        read_step<S, NMB>(w, ring, a0, a1, b0, b1);
+        // the reads of stage S complete before E_{j+1}, where it is refilled
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));
+    }
+}
+
+// The tile's epilogue for one wave: NMB row blocks of its 128-row half.
+template <bool SWIGLU, int NMB>
+__device__ __forceinline__ void store_tile(const f32x16 (&acc)[NMB > 0 ? NMB : 1][2], const GemmArgs &a,
+                                           int N, int n0, int row0, int rows_valid, bool sh, int wm,
+                                           int wn, int lane)
+{
+    if constexpr (NMB > 0) {
+        // transposed product: lane l holds token 32 mb + l % 32 of the wave's
+        // 128-row half (see store_block_bf16)
+        bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) {
+            const int tok = wm * 128 + mb * 32 + (lane & 31);
+            const bool valid = tok < rows_valid;
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                const int col = n0 + wn * 64 + nb * 32;
+                if constexpr (SWIGLU)
+                    store_block_swiglu(acc[mb][nb], C + (int64_t)(row0 + tok) * (N / 2) + col / 2,
+                                       valid);
+                else
+                    store_block_bf16(acc[mb][nb], C + (int64_t)(row0 + tok) * N + col,
+                                     valid && col < N);
+            }
+        }
+    }
+}
+
 // One tile for a wave whose 128-row half holds NMB non-empty 32-row blocks:
 // K loop, then the epilogue.  NMB = 0 only for the upper half of a tile of
 // at most 128 rows: the wave then loads no token rows (they are all past the
@@ -234,26 +360,40 @@ __device__ __forceinline__ void run_tile(const Tile &t, const WaveConst &w, cons
         kstep<3, NMB, STREAM>(t, w, ring, acc, j + 3);
     }
     __syncthreads();   // drain the look-ahead fills before the ring is reused
-    if constexpr (NMB > 0) {
-        // transposed product: lane l holds token 32 mb + l % 32 of the wave's
-        // 128-row half (see store_block_bf16)
-        bf16 *C = (bf16 *)(sh ? a.C_shared : a.C_routed);
+    store_tile<SWIGLU, NMB>(acc, a, N, n0, row0, rows_valid, sh, wm, wn, lane);
+}
+
+// A full tile (both halves hold four row blocks), K loop in two phases.
+template <bool SWIGLU, bool STREAM, bool LEAD>
+__device__ __forceinline__ void run_full_tile(const Tile &t, const WaveConst &w, const Stage (&ring)[4],
+                                              const GemmArgs &a, int N, int n0, int row0, bool sh,
+                                              int wm, int wn, int lane)
+{
+    f32x16 acc[4][2];
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb) {
-            const int tok = wm * 128 + mb * 32 + (lane & 31);
-            const bool valid = tok < rows_valid;
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
-                const int col = n0 + wn * 64 + nb * 32;
-                if constexpr (SWIGLU)
-                    store_block_swiglu(acc[mb][nb], C + (int64_t)(row0 + tok) * (N / 2) + col / 2,
-                                       valid);
-                else
-                    store_block_bf16(acc[mb][nb], C + (int64_t)(row0 + tok) * N + col,
-                                     valid && col < N);
-            }
-        }
+    for (int i = 0; i < 4; ++i) acc[i][0] = acc[i][1] = (f32x16){};
+    bf16x8 a0[4], a1[4], b0[2], b1[2];
+    fill<true, STREAM>(t, w, ring[0], 0);
+    fill<true, STREAM>(t, w, ring[1], 1);
+    fill<true, STREAM>(t, w, ring[2], 2);
+    // K is a multiple of 128, so KT is a multiple of 4; the first step (the
+    // trailing half has nothing to multiply yet), then branch-free bodies of
+    // four steps (stage = step % 4)
+    pp_step<0, 4, STREAM, LEAD, false>(t, w, ring, acc, a0, a1, b0, b1, 0);
+    pp_step<1, 4, STREAM, LEAD, true>(t, w, ring, acc, a0, a1, b0, b1, 1);
+    pp_step<2, 4, STREAM, LEAD, true>(t, w, ring, acc, a0, a1, b0, b1, 2);
+    pp_step<3, 4, STREAM, LEAD, true>(t, w, ring, acc, a0, a1, b0, b1, 3);
+    for (int j = 4; j < t.KT; j += 4) {
+        pp_step<0, 4, STREAM, LEAD, true>(t, w, ring, acc, a0, a1, b0, b1, j);
+        pp_step<1, 4, STREAM, LEAD, true>(t, w, ring, acc, a0, a1, b0, b1, j + 1);
+        pp_step<2, 4, STREAM, LEAD, true>(t, w, ring, acc, a0, a1, b0, b1, j + 2);
+        pp_step<3, 4, STREAM, LEAD, true>(t, w, ring, acc, a0, a1, b0, b1, j + 3);
     }
+    // E_KT: the trailing half multiplies the last step
+    phase_barrier();
+    if constexpr (!LEAD) mma_step<4, STREAM, false>(t, w, ring[0], 0, acc, a0, a1, b0, b1);
+    __syncthreads();   // drain the look-ahead fills before the ring is reused
+    store_tile<SWIGLU, 4>(acc, a, N, n0, row0, kBM, sh, wm, wn, lane);
 }
 
 }  // namespace
@@ -363,7 +503,16 @@ void k_gemm_bf16(GemmArgs a)
         // what the caches hold for later kernels (the combine's rows) and the
         // dirty lines of earlier ones.  Groups of several row tiles share
         // their panels through L2 and keep ordinary loads.
-        if (grows <= kBM) {
+        if (rows_valid == kBM) {
+            // every wave's half is full: the two-phase loop
+            if (grows <= kBM) {
+                if (wm == 0) run_full_tile<SWIGLU, true, true>(t, w, ring, a, N, n0, row0, sh, wm, wn, lane);
+                else run_full_tile<SWIGLU, true, false>(t, w, ring, a, N, n0, row0, sh, wm, wn, lane);
+            } else {
+                if (wm == 0) run_full_tile<SWIGLU, false, true>(t, w, ring, a, N, n0, row0, sh, wm, wn, lane);
+                else run_full_tile<SWIGLU, false, false>(t, w, ring, a, N, n0, row0, sh, wm, wn, lane);
+            }
+        } else if (grows <= kBM) {
             switch (nmb) {
             case 0: run_tile<SWIGLU, 0, true>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
             case 1: run_tile<SWIGLU, 1, true>(t, w, ring, a, N, n0, row0, rows_valid, sh, wm, wn, lane); break;
