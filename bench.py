@@ -42,9 +42,8 @@ def gemm_accounting(cfg, counts_local, T):
     """Algorithmic FLOPs and HBM bytes of one launch of each grouped GEMM.
 
     gate/up: 4 d f FLOP per row; reads each active expert's [2f, d] weights
-    once and every routed row once (bf16: the token row of x, found through
-    slot_of_row; fp8: the row of X_perm), and the shared expert's rows of x;
-    writes H.
+    once and every routed row once (the token row of x, found through
+    slot_of_row), and the shared expert's rows of x; writes H.
     down:    2 d f FLOP per row; reads [d, f] weights, H; writes Y.
     """
     d, f = cfg.d, cfg.f
@@ -70,9 +69,12 @@ def stream_accounting(cfg, counts_local, n_tokens_with_local, T):
     n_loc = int(counts_local.sum())
     rb = d * 2
     index = T * k * 4 + cfg.E * 4 + (cfg.E_loc + 1) * 4 + (n_loc + T * k) * 4
-    # the gather runs in fp8 mode only: e4m3 codes plus one fp32 scale per 128 channels
-    gb = d + (d // 128) * 4 if cfg.dtype == "fp8" else rb
-    gather = n_tokens_with_local * gb + n_loc * gb + n_loc * 4
+    # the gather runs in fp8 mode only and moves the token scales (one fp32
+    # per 128 channels; the GEMM reads the e4m3 rows of x itself): each
+    # token's scales read once, one row of scales written per routed row,
+    # plus slot_of_row
+    sb = (d // 128) * 4
+    gather = n_tokens_with_local * sb + n_loc * sb + n_loc * 4
     combine = T * k * 12 + n_loc * rb + T * rb + (T * rb if cfg.has_shared else 0)
     return dict(index_bytes=index, gather_bytes=gather, combine_bytes=combine)
 
@@ -295,6 +297,9 @@ def stream_rooflines(r):
             gbs = b / (t / 1e3) / 1e9
             out[k] = {"avg_ms": round(t, 4), "algorithmic_bytes": b, "achieved_GBs": round(gbs, 1),
                       "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+            if k == "gather":
+                # the fp8 token scales only (a few MB): launch and memory latency
+                out[k]["bound"] = "latency"
     g1, g2 = r["kern"][g1k], r["kern"][g2k]
     out[g1k] = {"avg_ms": round(g1, 4), "tflops": round(a["g1_flop"] / (g1 / 1e3) / 1e12, 1)}
     out[g2k] = {"avg_ms": round(g2, 4), "tflops": round(a["g2_flop"] / (g2 / 1e3) / 1e12, 1)}

@@ -51,11 +51,12 @@
  *   base_t         = 0 (MOE_COMBINE_OVERWRITE) or the previous out[t]
  *                    (MOE_COMBINE_ACCUMULATE), plus the shared expert's
  *                    output when the stage has one.
- * Intermediate rows (H, Y_perm) are stored in bf16 (fp8 mode: X_perm and H
- * as e4m3 with per-128-channel fp32 scales; h is quantised from its fp32
- * value by the rule of moe_quantize_fp8).  In bf16 mode X_perm is never
- * materialised: the gate/up grouped GEMM loads row r straight from
- * x[slot_of_row[r] / k] (the row gather is fused into its token-row loads).  The combine accumulates in
+ * Intermediate rows (H, Y_perm) are stored in bf16 (fp8 mode: H as e4m3
+ * with per-128-channel fp32 scales; h is quantised from its fp32 value by
+ * the rule of moe_quantize_fp8).  X_perm is never materialised: the gate/up
+ * grouped GEMM loads row r straight from x[slot_of_row[r] / k] (the row
+ * gather is fused into its token-row loads); in fp8 mode only the rows'
+ * scales are gathered, transposed, into x_perm_scales.  The combine accumulates in
  * fp32 and rounds once to bf16.  Tokens with no local slot are written as
  * +0.0 (overwrite) or left untouched (accumulate).  The combine uses no
  * atomics, so results are bit-identical from run to run and independent of
@@ -181,8 +182,8 @@ typedef struct {
     int32_t *offsets;         /* [E_loc + 1] */
     int32_t *slot_of_row;     /* [capacity_rows] */
     int32_t *row_of_slot;     /* [max_tokens * k] */
-    void    *x_perm;          /* fp8: [capacity_rows][d] e4m3; bf16: NULL (not materialised) */
-    float   *x_perm_scales;   /* fp8: [d/128][capacity_rows] (transposed) */
+    void    *x_perm;          /* NULL: the row gather is fused into the gate/up GEMM */
+    float   *x_perm_scales;   /* fp8: the routed rows' x scales, [d/128][capacity_rows] (transposed) */
     void    *h;               /* [capacity_rows][f] bf16 or e4m3 */
     float   *h_scales;        /* fp8: [f/128][capacity_rows] (transposed) */
     void    *y_perm;          /* [capacity_rows][d] bf16 */
@@ -206,9 +207,9 @@ MOE_API moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weight
 /* Waits for all work of the stage and frees it.  NULL is a no-op. */
 MOE_API void moe_stage_destroy(moe_stage *stage);
 
-/* Step 1 (histogram, scan, stable scatter; in fp8 mode also the row gather
- * of codes and scales into X_perm) on `slot`'s workspace.  Records the
- * micro-batch for the slot's later calls: in bf16 mode the gate/up GEMM of
+/* Step 1 (histogram, scan, stable scatter; in fp8 mode also the gather of
+ * the routed rows' scales into x_perm_scales) on `slot`'s workspace.  Records
+ * the micro-batch for the slot's later calls: the gate/up GEMM of
  * moe_expert_ffn reads the token rows from mb->x, which must stay valid until
  * the slot's work completes (as every micro-batch buffer must). */
 MOE_API moe_status moe_dispatch(moe_stage *stage, int32_t slot, const moe_microbatch *mb,

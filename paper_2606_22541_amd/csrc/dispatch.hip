@@ -1,5 +1,5 @@
 // Dispatch of one micro-batch: per-expert histogram, scan, stable counting-sort
-// scatter and coalesced row gather.
+// scatter and the gather of the fp8 token scales.
 //
 // The per-expert token counts are the metadata the paper's MoE devices receive
 // with each batch, and the payload is grouped by expert (section 3.2.1,
@@ -347,58 +347,52 @@ hipError_t launch_dispatch_index(const DispatchArgs &a, hipStream_t s)
 }
 
 // ---------------------------------------------------------------------------
-// 4. Row gather: one workgroup per row (grid-stride).  Thread tid moves the
-//    16-byte chunks c0 + 256 u + tid, u < U.  Chunk indices are clamped into
-//    the row rather than guarded, so that all U loads are issued before the
-//    first store; a clamped lane rewrites the row's last chunk with the same
-//    value, which is harmless for a pure copy.
+// 4. Scale gather (fp8): the grouped GEMMs read the token rows of x through
+//    slot_of_row themselves, but they take the step's token scales as one
+//    contiguous run per 128-channel group, so the scales of the routed rows
+//    are gathered here into the transposed [n_scales][scale_ld] layout.
+//    Work item i (grid-stride) moves the scales of groups 8 (i / n_rows) ..
+//    + 7 of row i % n_rows: the stores of a group are consecutive across a
+//    wave, and each thread has its eight loads in flight at once.
 // ---------------------------------------------------------------------------
 constexpr int kGatherThreads = 256;
+constexpr int kScalesPerItem = 8;
 
-template <int U>
 __global__ __launch_bounds__(kGatherThreads)
-void k_gather(const uint4 *__restrict__ x, const float *__restrict__ xs,
-              const int32_t *__restrict__ slot_of_row, const int32_t *__restrict__ n_rows_dev,
-              int32_t k, int32_t row_vecs, int32_t n_scales, uint4 *__restrict__ xp,
-              float *__restrict__ xps, int32_t scale_ld)
+void k_gather_scales(const float *__restrict__ xs, const int32_t *__restrict__ slot_of_row,
+                     const int32_t *__restrict__ n_rows_dev, int32_t k, int32_t n_scales,
+                     float *__restrict__ xps, int32_t scale_ld)
 {
     const int n_rows = *n_rows_dev;
-    for (int r = blockIdx.x; r < n_rows; r += gridDim.x) {
-        const int t = slot_of_row[r] / k;
-        const uint4 *src = x + (int64_t)t * row_vecs;
-        uint4 *dst = xp + (int64_t)r * row_vecs;
-        for (int c0 = 0; c0 < row_vecs; c0 += kGatherThreads * U) {
-            int cc[U];
-            uint4 v[U];
+    if (n_rows <= 0) return;
+    const int64_t chunks = (n_scales + kScalesPerItem - 1) / kScalesPerItem;
+    const int64_t total = (int64_t)n_rows * chunks;
+    for (int64_t i = (int64_t)blockIdx.x * kGatherThreads + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * kGatherThreads) {
+        const int c = (int)(i / n_rows);
+        const int r = (int)(i - (int64_t)c * n_rows);
+        const int g0 = c * kScalesPerItem;
+        const float *src = xs + (int64_t)(slot_of_row[r] / k) * n_scales;
+        float v[kScalesPerItem];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                cc[u] = min(c0 + u * kGatherThreads + (int)threadIdx.x, row_vecs - 1);
-                v[u] = src[cc[u]];
-            }
+        for (int u = 0; u < kScalesPerItem; ++u) v[u] = src[min(g0 + u, n_scales - 1)];
 #pragma unroll
-            for (int u = 0; u < U; ++u) dst[cc[u]] = v[u];
-        }
-        if (xs != nullptr)
-            for (int c = threadIdx.x; c < n_scales; c += kGatherThreads)
-                xps[(int64_t)c * scale_ld + r] = xs[(int64_t)t * n_scales + c];
+        for (int u = 0; u < kScalesPerItem; ++u)
+            if (g0 + u < n_scales) xps[(int64_t)(g0 + u) * scale_ld + r] = v[u];
     }
 }
 
-hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_t *slot_of_row,
-                              const int32_t *n_rows_dev, int32_t k, int32_t row_bytes,
-                              int32_t n_scales, void *x_perm, float *x_perm_scales,
-                              int32_t scale_ld, int32_t max_rows, int num_cus, hipStream_t s)
+hipError_t launch_gather_scales(const float *x_scales, const int32_t *slot_of_row,
+                                const int32_t *n_rows_dev, int32_t k, int32_t n_scales,
+                                float *x_perm_scales, int32_t scale_ld, int32_t max_rows,
+                                int num_cus, hipStream_t s)
 {
-    if (max_rows <= 0) return hipSuccess;
-    int grid = num_cus * 16;
-    if (grid > max_rows) grid = max_rows;
-    const int row_vecs = row_bytes / 16;
-    auto kern = row_vecs > 2 * kGatherThreads ? k_gather<4>
-              : row_vecs > kGatherThreads     ? k_gather<2>
-                                              : k_gather<1>;
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kGatherThreads), 0, s, (const uint4 *)x, x_scales,
-                       slot_of_row, n_rows_dev, k, row_vecs, n_scales, (uint4 *)x_perm,
-                       x_perm_scales, scale_ld);
+    if (max_rows <= 0 || n_scales <= 0) return hipSuccess;
+    const int64_t work = (int64_t)max_rows * ((n_scales + kScalesPerItem - 1) / kScalesPerItem);
+    int64_t grid = (work + kGatherThreads - 1) / kGatherThreads;
+    if (grid > (int64_t)num_cus * 4) grid = (int64_t)num_cus * 4;
+    hipLaunchKernelGGL(k_gather_scales, dim3((unsigned)grid), dim3(kGatherThreads), 0, s, x_scales,
+                       slot_of_row, n_rows_dev, k, n_scales, x_perm_scales, scale_ld);
     return hipGetLastError();
 }
 

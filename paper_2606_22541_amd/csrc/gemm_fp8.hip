@@ -46,6 +46,11 @@
 //    range and read as zero; the scalar offset, which the range check does
 //    not cover, only moves along K (clamped to the last group) and between
 //    weight fragments that exist;
+//  * the gate/up product reads the routed token rows straight from x through
+//    slot_of_row (the row gather is part of the token fills, as in bf16); the
+//    rows' fp32 scales arrive already gathered and transposed, one
+//    contiguous run of 128 per group, since reading them per token would cost
+//    one cache line per lane and load;
 //  * SwiGLU mode: every wave forms h = SiLU(gate) * up in fp32 for its 32
 //    channels, the per-token |h| maximum over the tile's 128 channels meets
 //    in a 2 KB LDS table, and each token's channels are quantised to e4m3
@@ -424,7 +429,12 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
         const int rows_valid = min(kTokT, grows - mt * kTokT);
         const int n0 = nt * kFeatT;
         const bool sh = (g == a.shared_group);
-        const uint8_t *A = (const uint8_t *)(sh ? a.A_shared : a.A_routed) + (int64_t)row0 * K;
+        // routed rows of an indexed A are gathered in the token fills: tile
+        // row r is row A_index[row0 + r] / A_index_div of the whole A (its
+        // scales are already gathered, indexed by the routed row)
+        const bool indexed = a.A_index != nullptr && !sh;
+        const uint8_t *A = indexed ? (const uint8_t *)a.A_routed
+                                   : (const uint8_t *)(sh ? a.A_shared : a.A_routed) + (int64_t)row0 * K;
         const float *As = (sh ? a.As_shared : a.As_routed) + row0;      // [K/128][ld]
         const uint8_t *B = (const uint8_t *)Bw + ((int64_t)g * N + n0) * K;
         Tile8 t;
@@ -433,12 +443,13 @@ void k_gemm_fp8(GemmArgs a, int32_t lds_rows_routed, int32_t lds_rows_shared)
         t.ncb = min(kFeatT, N - n0) / 16;
         t.cbstride = t.KT * 2048;
         t.rw = rsrc8(B, (int64_t)t.ncb * t.cbstride);
-        t.rx = rsrc8(A, (int64_t)rows_valid * K);
+        t.rx = rsrc8(A, (indexed ? a.A_routed_rows : (int64_t)rows_valid) * K);
         t.rs = rsrc8(As, ((int64_t)(t.KT - 1) * t.s_ld + rows_valid) * 4);
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int r = frow + 8 * i;
-            t.vx[i] = r < rows_valid ? r * K + fch[i] : (int)0x80000000u;
+            t.vx[i] = r < rows_valid ? (indexed ? a.A_index[row0 + r] / a.A_index_div : r) * K + fch[i]
+                                     : (int)0x80000000u;
         }
         const float *sbp0, *sbp1;
         if constexpr (SWIGLU) {

@@ -34,14 +34,15 @@ hipError_t launch_group_tables_from_counts(const int32_t *counts, int32_t E_loc,
                                            int32_t n_rows_max, GroupTable g, int32_t *err,
                                            hipStream_t s);
 
-// X_perm[r] = x[slot_of_row[r] / k] for r < offsets[E_loc].  row_bytes is the
-// byte length of one activation row (2d for bf16, d for e4m3); when
-// scales != nullptr the row's fp32 scales (n_scales per row, row-major
-// [T][n_scales]) move as well and are stored transposed: [n_scales][scale_ld].
-hipError_t launch_gather_rows(const void *x, const float *x_scales, const int32_t *slot_of_row,
-                              const int32_t *n_rows_dev, int32_t k, int32_t row_bytes,
-                              int32_t n_scales, void *x_perm, float *x_perm_scales,
-                              int32_t scale_ld, int32_t max_rows, int num_cus, hipStream_t s);
+// fp8: the token scales of the routed rows, transposed: x_perm_scales[g *
+// scale_ld + r] = x_scales[(slot_of_row[r] / k) * n_scales + g] for r <
+// *n_rows_dev (offsets[E_loc]) and g < n_scales; max_rows bounds the rows
+// (grid size only).  The e4m3 rows themselves are read by the gate/up GEMM
+// through slot_of_row.
+hipError_t launch_gather_scales(const float *x_scales, const int32_t *slot_of_row,
+                                const int32_t *n_rows_dev, int32_t k, int32_t n_scales,
+                                float *x_perm_scales, int32_t scale_ld, int32_t max_rows,
+                                int num_cus, hipStream_t s);
 
 // [rows][cols] -> [cols][ld] copy of fp32 scales.
 hipError_t launch_transpose_scales(const float *src, int32_t rows, int32_t cols, float *dst,
@@ -70,9 +71,11 @@ struct GemmArgs {
     GroupTable groups;
     int32_t G;
     int32_t large_all;       // bf16 256x256 kernel: 1 = every group, 0 = only rows > kSmallRows
-    // bf16 only: when A_index is set, routed row r (r < the routed rows) is row
+    // When A_index is set, routed row r (r < the routed rows) is row
     // A_index[r] / A_index_div of A_routed, which has A_routed_rows rows (the
     // row gather happens in the GEMM's token-row loads; A_index = slot_of_row).
+    // In fp8 the A scales stay indexed by the routed row (As_routed holds the
+    // gathered scales, launch_gather_scales).
     const int32_t *A_index;
     int32_t A_index_div;
     int64_t A_routed_rows;

@@ -111,7 +111,7 @@ Sizes sizes_of(const moe_stage_desc *d)
     b += align256(s.nb_max * E * 4) + align256(E * 4) + align256((El + 1) * 4);
     b += 2 * align256(s.G * 4) + 7 * align256((s.G + 1) * 4);
     b += align256(cap1 * 4) + align256((s.n_slots_tok > 0 ? s.n_slots_tok : 1) * 4);
-    if (fp8) b += align256(cap1 * D) + align256(cap1 * (D / 128) * 4);   // X_perm (fp8 only)
+    if (fp8) b += align256(cap1 * (D / 128) * 4);   // gathered token scales (fp8 only)
     b += align256(cap1 * F * s.eb) + (fp8 ? align256(cap1 * (F / 128) * 4) : 0);
     b += align256(cap1 * D * 2);
     if (d->has_shared_expert) {
@@ -376,10 +376,9 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
              alloc(st, &sl.row_of_slot, (z.n_slots_tok > 0 ? z.n_slots_tok : 1) * 4) &&
              alloc(st, &sl.h, cap1 * F * z.eb) &&
              alloc(st, &sl.y_perm, cap1 * D * 2);
-        // X_perm exists only in fp8 mode; in bf16 the gate/up GEMM gathers the
-        // token rows itself
-        if (ok && fp8) ok = alloc(st, &sl.x_perm, cap1 * D) &&
-                            alloc(st, &sl.x_perm_s, cap1 * (D / 128) * 4) &&
+        // no X_perm: the gate/up GEMM gathers the token rows itself; fp8 keeps
+        // the gathered token scales
+        if (ok && fp8) ok = alloc(st, &sl.x_perm_s, cap1 * (D / 128) * 4) &&
                             alloc(st, &sl.h_s, cap1 * (F / 128) * 4);
         if (ok && desc->has_shared_expert) {
             ok = alloc(st, &sl.h_sh, T1 * F * z.eb) && alloc(st, &sl.y_sh, T1 * D * 2);
@@ -472,15 +471,14 @@ static moe_status dispatch_impl(moe_stage *st, int32_t slot, const moe_microbatc
         ProfScope ps(st, 0, s);
         if (launch_dispatch_index(a, s) != hipSuccess) return MOE_EHIP;
     }
-    // fp8: gather the e4m3 rows and their (transposed) scales into X_perm.
-    // bf16: the gate/up GEMM reads the token rows of x through slot_of_row.
+    // The gate/up GEMM reads the token rows of x through slot_of_row; fp8
+    // gathers the rows' scales (transposed) for it.
     const int64_t max_rows = (int64_t)T * d.top_k;
     if (fp8 && max_rows > 0) {
         ProfScope ps(st, 1, s);
-        if (launch_gather_rows(mb->x, mb->x_scales, sl.slot_of_row,
-                               sl.offsets + d.n_local_experts, d.top_k, d.d_model,
-                               d.d_model / 128, sl.x_perm, sl.x_perm_s, (int32_t)st->sz.cap,
-                               (int32_t)max_rows, stream_cus(st, s), s) != hipSuccess)
+        if (launch_gather_scales(mb->x_scales, sl.slot_of_row, sl.offsets + d.n_local_experts,
+                                 d.top_k, d.d_model / 128, sl.x_perm_s, (int32_t)st->sz.cap,
+                                 (int32_t)max_rows, stream_cus(st, s), s) != hipSuccess)
             return MOE_EHIP;
         if (fp8 && d.has_shared_expert &&
             launch_transpose_scales(mb->x_scales, T, d.d_model / 128, sl.xsh_s, d.max_tokens,
@@ -545,13 +543,11 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     if (d.has_shared_expert) mt_max += (T + kBM - 1) / kBM;
 
     GemmArgs g1{};
-    g1.A_routed = fp8 ? sl.x_perm : sl.mb.x;
+    g1.A_routed = sl.mb.x;           // routed row r = token slot_of_row[r] / k of x
     g1.A_shared = sl.mb.x;
-    if (!fp8) {                      // routed row r = token slot_of_row[r] / k of x
-        g1.A_index = sl.slot_of_row;
-        g1.A_index_div = d.top_k;
-        g1.A_routed_rows = T;
-    }
+    g1.A_index = sl.slot_of_row;
+    g1.A_index_div = d.top_k;
+    g1.A_routed_rows = T;
     g1.As_routed = sl.x_perm_s;
     g1.As_shared = sl.xsh_s;
     g1.B = st->w1;

@@ -47,7 +47,7 @@ NAME_MAP = (
     ("void moe::k_gemm_fp8<true>", "gemm_gate_up_swiglu_fp8"),
     ("void moe::k_gemm_fp8<false>", "gemm_down_fp8"),
     ("moe::k_combine", "combine"),
-    ("void moe::k_gather", "gather"),
+    ("moe::k_gather_scales", "gather"),
     ("moe::k_hist", "dispatch_index"),
     ("moe::k_place", "dispatch_index"),
     ("moe::k_quantize_fp8", "quantize_fp8"),

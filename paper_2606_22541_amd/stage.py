@@ -97,7 +97,7 @@ class ExpertStage:
         res["row_of_slot"] = device_to_numpy(v.row_of_slot, T * cfg.k, np.int32)
         if rows:
             eb = np.uint8 if self.fp8 else np.uint16
-            if v.x_perm:          # bf16 mode fuses the row gather into the GEMM
+            if v.x_perm:          # NULL: the row gather is fused into the gate/up GEMM
                 res["x_perm"] = device_to_numpy(v.x_perm, n * cfg.d, eb).reshape(n, cfg.d)
             res["h"] = device_to_numpy(v.h, n * cfg.f, eb).reshape(n, cfg.f)
             res["y_perm"] = device_to_numpy(v.y_perm, n * cfg.d, np.uint16).reshape(n, cfg.d)

@@ -65,10 +65,11 @@ def check_dispatch(view, ref, cfg, mb=None):
     if mb is not None and "x_perm" in view and cfg.dtype == "bf16":
         src = bf16_bits(mb.x)[ref["slot_of_row"] // cfg.k]
         assert np.array_equal(view["x_perm"], src), "X_perm is not an exact row gather"
-    if mb is not None and "x_perm" in view and cfg.dtype == "fp8":
+    if mb is not None and "x_perm_scales" in view and cfg.dtype == "fp8":
+        # the e4m3 rows are read by the gate/up GEMM through slot_of_row (checked
+        # through H and Y_perm); their scales are gathered, bit-exact
         tok = ref["slot_of_row"] // cfg.k
-        assert np.array_equal(view["x_perm"], ref["x_codes"][tok]), "fp8 X_perm codes differ"
-        assert np.array_equal(view["x_perm_scales"], ref["x_scales"][tok]), "fp8 X_perm scales differ"
+        assert np.array_equal(view["x_perm_scales"], ref["x_scales"][tok]), "fp8 gathered x scales differ"
 
 
 def row_rel_l2(got, want):

@@ -71,10 +71,10 @@ def test_workspace_bytes_host_only(lib):
     f_slot = (f3 - f1) // 2
     # fp8 weights: one byte per element plus one fp32 scale per 128x128 block
     assert 8 * 3 * 2048 * 7168 <= f1 - f_slot < weights
-    # fp8 slots: X_perm (d bytes per row) and its scales, H (f bytes) and its
-    # scales, Y_perm (2d bytes); h is quantised inside the gate/up GEMM, so no
-    # bf16 copy of H is kept
-    fp8_row = 7168 + 7168 // 128 * 4 + 2048 + 2048 // 128 * 4 + 7168 * 2
+    # fp8 slots: the gathered x scales (no X_perm: the gate/up GEMM reads the
+    # e4m3 rows of x itself), H (f bytes) and its scales, Y_perm (2d bytes);
+    # h is quantised inside the gate/up GEMM, so no bf16 copy of H is kept
+    fp8_row = 7168 // 128 * 4 + 2048 + 2048 // 128 * 4 + 7168 * 2
     assert rows * fp8_row <= f_slot < rows * fp8_row + 8 * 2**20
 
 

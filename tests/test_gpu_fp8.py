@@ -1,8 +1,10 @@
 """GPU parity of the fp8 (e4m3, 128-block scales) expert stage and of the
 sender-side quantiser against the CPU oracle.
 
-Bit-exact: quantiser codes and scales, counts, permutation, X_perm codes and
-scales.  Floating point: rel-L2 <= 3e-2 on outputs and per expert on Y_perm.
+Bit-exact: quantiser codes and scales, counts, permutation, the gathered x
+scales (the e4m3 rows themselves are read by the gate/up GEMM through
+slot_of_row and checked through H and Y_perm).  Floating point: rel-L2 <= 3e-2
+on outputs and per expert on Y_perm.
 """
 import numpy as np
 import pytest
