@@ -43,23 +43,43 @@ constexpr int kErrBadCount = 8;       // pre-grouped counts negative or past the
 // small-group GEMM, which streams each weight panel exactly once; larger
 // groups use the 256x256-tile GEMM.
 constexpr int kSmallRows = 192;
+// The down product's partition: only groups of at most this many rows take
+// the small-group kernel (at ~130 rows per expert, 256-wide tiles of the down
+// product's d columns fill the GPU in one round, where 128-wide small tiles
+// would take 1.75 rounds; groups of a few dozen rows, as the cold experts of
+// skewed routing have, stream their weights faster in the small kernel).
+constexpr int kSmallRowsDown = 64;
 
 // Device-side tables written by the dispatch scan, read by the GEMMs.
 struct GroupTable {
     int32_t *row0;      // [G] first row of the group in its A matrix
     int32_t *rows;      // [G] rows of the group
-    int32_t *mt_base;   // [G+1] prefix of ceil(rows / kBM) over all groups
-    int32_t *lt_base;   // [G+1] same, counting only groups with rows > kSmallRows
+    int32_t *lt_base;   // [G+1] prefix of ceil(rows / kBM) over groups with rows > kSmallRows
     int32_t *st_base;   // [G+1] prefix of 1 per group with 1 <= rows <= kSmallRows
     // Tile order of the 256-row bf16 GEMM: the full row tiles of every group
     // first, then the partial ones (rows % kBM != 0), largest first, so the
     // cheap partial tiles fill the last round of the persistent grid.
-    int32_t *fm_base;   // [G+1] prefix of rows / kBM over all groups
-    int32_t *fl_base;   // [G+1] same, over groups with rows > kSmallRows
-    int32_t *pm_list;   // [G+1] groups with a partial row tile, by descending
-                        //       rows % kBM (ties: lower index first); count at [G]
-    int32_t *pl_list;   // [G+1] same, over groups with rows > kSmallRows
+    int32_t *fl_base;   // [G+1] prefix of rows / kBM over groups with rows > kSmallRows
+    int32_t *pl_list;   // [G+1] groups with rows > kSmallRows and a partial row tile,
+                        //       by descending rows % kBM (ties: lower index first); count at [G]
+    // The same partition at kSmallRowsDown rows (the down product's):
+    int32_t *lt_base_d; // [G+1] as lt_base, groups with rows > kSmallRowsDown
+    int32_t *st_base_d; // [G+1] as st_base, groups with 1 <= rows <= kSmallRowsDown
+    int32_t *fl_base_d; // [G+1] as fl_base, groups with rows > kSmallRowsDown
+    int32_t *pl_list_d; // [G+1] as pl_list, groups with rows > kSmallRowsDown
 };
+
+// The tables a GEMM launch reads for the down product: the partition at
+// kSmallRowsDown in place of the one at kSmallRows.
+__host__ __device__ inline GroupTable down_partition(const GroupTable &g)
+{
+    GroupTable d = g;
+    d.lt_base = g.lt_base_d;
+    d.st_base = g.st_base_d;
+    d.fl_base = g.fl_base_d;
+    d.pl_list = g.pl_list_d;
+    return d;
+}
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 

@@ -97,61 +97,67 @@ __device__ void build_group_tables(const GroupTable &g, const int32_t *tot, int 
                                    int has_shared, int T, int lane)
 {
     const int G = E_loc + (has_shared ? 1 : 0);
-    int c_row = 0, c_mt = 0, c_lt = 0, c_st = 0, c_fm = 0, c_fl = 0, c_pm = 0, c_pl = 0;
+    int c_row = 0;
+    int c_lt[2] = {0, 0}, c_st[2] = {0, 0}, c_fl[2] = {0, 0}, c_pl[2] = {0, 0};
+    int32_t *lt_base[2] = {g.lt_base, g.lt_base_d}, *st_base[2] = {g.st_base, g.st_base_d};
+    int32_t *fl_base[2] = {g.fl_base, g.fl_base_d}, *pl_list[2] = {g.pl_list, g.pl_list_d};
+    constexpr int kThresh[2] = {kSmallRows, kSmallRowsDown};
     for (int c0 = 0; c0 < G; c0 += 64) {
         const int i = c0 + lane;
         const int rows = i < E_loc ? tot[i] : (i < G ? T : 0);
         const int m = (rows + kBM - 1) / kBM;
-        const bool large = rows > kSmallRows;
         const int fm = rows / kBM, rem = rows - fm * kBM;
-        int t_row, t_mt, t_lt, t_st, t_fm, t_fl, t_pm, t_pl;
+        int t_row;
         const int p_row = wave_excl_scan(i < E_loc ? rows : 0, lane, t_row);
-        const int p_mt = wave_excl_scan(m, lane, t_mt);
-        const int p_lt = wave_excl_scan(large ? m : 0, lane, t_lt);
-        const int p_st = wave_excl_scan(rows > 0 && !large ? 1 : 0, lane, t_st);
-        const int p_fm = wave_excl_scan(fm, lane, t_fm);
-        const int p_fl = wave_excl_scan(large ? fm : 0, lane, t_fl);
-        wave_excl_scan(rem > 0 ? 1 : 0, lane, t_pm);
-        wave_excl_scan(rem > 0 && large ? 1 : 0, lane, t_pl);
         if (i < G) {
             g.row0[i] = i < E_loc ? c_row + p_row : 0;
             g.rows[i] = rows;
-            g.mt_base[i] = c_mt + p_mt;
-            g.lt_base[i] = c_lt + p_lt;
-            g.st_base[i] = c_st + p_st;
-            g.fm_base[i] = c_fm + p_fm;
-            g.fl_base[i] = c_fl + p_fl;
-            if (rem > 0) {
-                // rank among the partial row tiles: more rows first, then lower index
-                int rank_m = 0, rank_l = 0;
-                for (int j = 0; j < G; ++j) {
-                    const int rj = j < E_loc ? tot[j] : T;
-                    const int qj = rj % kBM;
-                    const bool before = qj > 0 && (qj > rem || (qj == rem && j < i));
-                    rank_m += before ? 1 : 0;
-                    rank_l += (before && rj > kSmallRows) ? 1 : 0;
-                }
-                g.pm_list[rank_m] = i;
-                if (large) g.pl_list[rank_l] = i;
+        }
+        // the two partitions into small groups (the small-group kernel) and
+        // large ones (the 256-row kernel): gate/up at kSmallRows, down at
+        // kSmallRowsDown
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const bool large = rows > kThresh[q];
+            int t_lt, t_st, t_fl, t_pl;
+            const int p_lt = wave_excl_scan(large ? m : 0, lane, t_lt);
+            const int p_st = wave_excl_scan(rows > 0 && !large ? 1 : 0, lane, t_st);
+            const int p_fl = wave_excl_scan(large ? fm : 0, lane, t_fl);
+            wave_excl_scan(rem > 0 && large ? 1 : 0, lane, t_pl);
+            if (i < G) {
+                lt_base[q][i] = c_lt[q] + p_lt;
+                st_base[q][i] = c_st[q] + p_st;
+                fl_base[q][i] = c_fl[q] + p_fl;
             }
+            c_lt[q] += t_lt;
+            c_st[q] += t_st;
+            c_fl[q] += t_fl;
+            c_pl[q] += t_pl;
+        }
+        if (i < G && rem > 0) {
+            // rank among the large groups' partial row tiles: more rows first,
+            // then lower index
+            int rank_l[2] = {0, 0};
+            for (int j = 0; j < G; ++j) {
+                const int rj = j < E_loc ? tot[j] : T;
+                const int qj = rj % kBM;
+                const bool before = qj > 0 && (qj > rem || (qj == rem && j < i));
+                rank_l[0] += (before && rj > kThresh[0]) ? 1 : 0;
+                rank_l[1] += (before && rj > kThresh[1]) ? 1 : 0;
+            }
+            if (rows > kThresh[0]) pl_list[0][rank_l[0]] = i;
+            if (rows > kThresh[1]) pl_list[1][rank_l[1]] = i;
         }
         c_row += t_row;
-        c_mt += t_mt;
-        c_lt += t_lt;
-        c_st += t_st;
-        c_fm += t_fm;
-        c_fl += t_fl;
-        c_pm += t_pm;
-        c_pl += t_pl;
     }
     if (lane == 0) {
-        g.mt_base[G] = c_mt;
-        g.lt_base[G] = c_lt;
-        g.st_base[G] = c_st;
-        g.fm_base[G] = c_fm;
-        g.fl_base[G] = c_fl;
-        g.pm_list[G] = c_pm;
-        g.pl_list[G] = c_pl;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            lt_base[q][G] = c_lt[q];
+            st_base[q][G] = c_st[q];
+            fl_base[q][G] = c_fl[q];
+            pl_list[q][G] = c_pl[q];
+        }
     }
 }
 

@@ -59,8 +59,9 @@
 //    matrix packs gate and up rows in interleaved blocks of 16, so a lane's
 //    registers r and r + 8 of a 32-column block are gate and up of the same
 //    h column (store_block_swiglu);
-//  * for the gate/up product, groups of at most kSmallRows rows are left to
-//    the small-group kernel (large_all = 0).
+//  * groups of at most kSmallRows rows (gate/up) or kSmallRowsDown rows
+//    (down) are left to the small-group kernel: the launch's group tables
+//    (lt_base, fl_base, pl_list) count only the other groups.
 #include "kernels.h"
 
 namespace moe {
@@ -83,17 +84,17 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, in
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, n, 0x00020000);
 }
 
-__device__ __forceinline__ void decode_tile(int L, const int32_t *__restrict__ mt_base, int G,
+__device__ __forceinline__ void decode_tile(int L, const int32_t *__restrict__ tbase, int G,
                                             int NT, int &g, int &mt, int &nt)
 {
-    int lo = 0, hi = G;   // largest g with mt_base[g] * NT <= L
+    int lo = 0, hi = G;   // largest g with tbase[g] * NT <= L
     while (hi - lo > 1) {
         int mid = (lo + hi) >> 1;
-        if (mt_base[mid] * NT <= L) lo = mid; else hi = mid;
+        if (tbase[mid] * NT <= L) lo = mid; else hi = mid;
     }
     g = lo;
-    const int Lg = L - mt_base[g] * NT;
-    const int Mt = mt_base[g + 1] - mt_base[g];
+    const int Lg = L - tbase[g] * NT;
+    const int Mt = tbase[g + 1] - tbase[g];
     const int band = Lg / (kBandM * NT);
     const int r = Lg - band * kBandM * NT;
     const int bm = min(kBandM, Mt - band * kBandM);
@@ -419,7 +420,7 @@ void k_gemm_bf16(GemmArgs a)
     const int wm = w.wave >> 2, wn = w.wave & 3;        // 2 x 4 waves, 128 x 64 each
     const int N = a.N, K = a.K;
     const int NT = (N + kBN - 1) / kBN;
-    const int32_t *tbase = a.large_all ? a.groups.mt_base : a.groups.lt_base;
+    const int32_t *tbase = a.groups.lt_base;
     const int total = __builtin_amdgcn_readfirstlane(tbase[a.G] * NT);
     const int P = gridDim.x;
     const int first = (P & 7) ? (int)blockIdx.x : (int)((blockIdx.x & 7) * (P >> 3) + (blockIdx.x >> 3));
@@ -437,8 +438,8 @@ void k_gemm_bf16(GemmArgs a)
     // tiles that share its weight panels in L2.
     const int tail = total % P;
     const bool by_size = total <= P || (tail != 0 && 2 * tail <= P);
-    const int32_t *fbase = a.large_all ? a.groups.fm_base : a.groups.fl_base;
-    const int32_t *plist = a.large_all ? a.groups.pm_list : a.groups.pl_list;
+    const int32_t *fbase = a.groups.fl_base;
+    const int32_t *plist = a.groups.pl_list;
     const int n_full = by_size ? __builtin_amdgcn_readfirstlane(fbase[a.G] * NT) : total;
 
     // token fill: lane l covers row 32 w + l / 4 (+16 for the second

@@ -70,7 +70,6 @@ struct GemmArgs {
     int32_t shared_group;    // index of the shared group, -1 if none
     GroupTable groups;
     int32_t G;
-    int32_t large_all;       // bf16 256x256 kernel: 1 = every group, 0 = only rows > kSmallRows
     // When A_index is set, routed row r (r < the routed rows) is row
     // A_index[r] / A_index_div of A_routed, which has A_routed_rows rows (the
     // row gather happens in the GEMM's token-row loads; A_index = slot_of_row).
@@ -135,10 +134,9 @@ hipError_t launch_gemm_bf16_small(const GemmArgs &a, bool swiglu, int g_max, int
 // e4m3 grouped GEMM with 128-block scales (same conventions; the A scales
 // are transposed, [K/128][ld] with ld = lds_rows_routed / lds_rows_shared).
 // swiglu = true writes e4m3 h with one scale per row and 128 channels
-// (C and Cs, the scales transposed like the A scales).  Groups of
-// 1..kSmallRows rows run as one 192-row tile each (g_max bounds the group
-// count), the others as 256-row tiles (mt_max bounds those); with
-// large_all every group takes 256-row tiles.
+// (C and Cs, the scales transposed like the A scales).  Every group runs
+// as 128-row tiles (mt_max bounds the 256-row tiles of all groups together;
+// g_max is unused).
 hipError_t launch_gemm_fp8(const GemmArgs &a, bool swiglu, int mt_max, int g_max, int num_cus,
                            int32_t lds_rows_routed, int32_t lds_rows_shared, hipStream_t s);
 

@@ -25,9 +25,10 @@ namespace {
 
 // Histogram rows: ceil(T*k / 1024) rows of n_experts counts.
 constexpr int64_t kHistInts = int64_t(1) << 20;                  // 4 MiB
-// Tile tables: two arrays of G and seven of G + 1 entries, G <= 256.
+// Tile tables: two arrays of G and eight of G + 1 entries, G <= 256.
 constexpr int64_t kTableStride = kMaxLocalExperts + 64;          // >= G + 1, 256-byte multiple
-constexpr int64_t kTableInts = 9 * kTableStride;
+constexpr int kTables = 10;
+constexpr int64_t kTableInts = kTables * kTableStride;
 constexpr int64_t kErrInts = 64;                                 // the fallback error word
 constexpr int64_t kScratchInts = kHistInts + kTableInts + kErrInts;
 constexpr int kMaxDevices = 64;
@@ -102,7 +103,8 @@ extern "C" moe_status moe_dispatch_index_noalloc(const int32_t *topk_ids, int32_
                           tables + 2 * kTableStride, tables + 3 * kTableStride,
                           tables + 4 * kTableStride, tables + 5 * kTableStride,
                           tables + 6 * kTableStride, tables + 7 * kTableStride,
-                          tables + 8 * kTableStride};
+                          tables + 8 * kTableStride, tables + 9 * kTableStride};
+    static_assert(kTables == 10, "one array per GroupTable member");
     a.slot_of_row = slot_of_row;
     a.row_of_slot = row_of_slot;
     a.err = err ? err : base + kHistInts + kTableInts;

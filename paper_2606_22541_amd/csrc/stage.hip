@@ -21,9 +21,16 @@ namespace {
 
 struct SlotWs {
     int32_t *blk_counts = nullptr, *counts = nullptr, *offsets = nullptr;
-    int32_t *g_row0 = nullptr, *g_rows = nullptr, *g_mt_base = nullptr;
+    int32_t *g_row0 = nullptr, *g_rows = nullptr;
     int32_t *g_lt_base = nullptr, *g_st_base = nullptr;
-    int32_t *g_fm_base = nullptr, *g_fl_base = nullptr, *g_pm_list = nullptr, *g_pl_list = nullptr;
+    int32_t *g_fl_base = nullptr, *g_pl_list = nullptr;
+    int32_t *g_lt_base_d = nullptr, *g_st_base_d = nullptr, *g_fl_base_d = nullptr,
+            *g_pl_list_d = nullptr;
+    GroupTable tables() const
+    {
+        return GroupTable{g_row0,    g_rows,      g_lt_base,   g_st_base,   g_fl_base,
+                          g_pl_list, g_lt_base_d, g_st_base_d, g_fl_base_d, g_pl_list_d};
+    }
     int32_t *slot_of_row = nullptr, *row_of_slot = nullptr;
     void *x_perm = nullptr;
     float *x_perm_s = nullptr;
@@ -109,7 +116,7 @@ Sizes sizes_of(const moe_stage_desc *d)
     const int64_t T1 = T > 0 ? T : 1;
     int64_t b = 0;
     b += align256(s.nb_max * E * 4) + align256(E * 4) + align256((El + 1) * 4);
-    b += 2 * align256(s.G * 4) + 7 * align256((s.G + 1) * 4);
+    b += 2 * align256(s.G * 4) + 8 * align256((s.G + 1) * 4);
     b += align256(cap1 * 4) + align256((s.n_slots_tok > 0 ? s.n_slots_tok : 1) * 4);
     if (fp8) b += align256(cap1 * (D / 128) * 4);   // gathered token scales (fp8 only)
     b += align256(cap1 * F * s.eb) + (fp8 ? align256(cap1 * (F / 128) * 4) : 0);
@@ -369,10 +376,11 @@ moe_status moe_stage_create(const moe_stage_desc *desc, const moe_weights *w, mo
         ok = alloc(st, &sl.blk_counts, z.nb_max * E * 4) && alloc(st, &sl.counts, E * 4) &&
              alloc(st, &sl.offsets, (El + 1) * 4) &&
              alloc(st, &sl.g_row0, z.G * 4) && alloc(st, &sl.g_rows, z.G * 4) &&
-             alloc(st, &sl.g_mt_base, (z.G + 1) * 4) && alloc(st, &sl.g_lt_base, (z.G + 1) * 4) &&
-             alloc(st, &sl.g_st_base, (z.G + 1) * 4) && alloc(st, &sl.g_fm_base, (z.G + 1) * 4) &&
-             alloc(st, &sl.g_fl_base, (z.G + 1) * 4) && alloc(st, &sl.g_pm_list, (z.G + 1) * 4) &&
-             alloc(st, &sl.g_pl_list, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
+             alloc(st, &sl.g_lt_base, (z.G + 1) * 4) && alloc(st, &sl.g_st_base, (z.G + 1) * 4) &&
+             alloc(st, &sl.g_fl_base, (z.G + 1) * 4) &&
+             alloc(st, &sl.g_pl_list, (z.G + 1) * 4) && alloc(st, &sl.g_lt_base_d, (z.G + 1) * 4) &&
+             alloc(st, &sl.g_st_base_d, (z.G + 1) * 4) && alloc(st, &sl.g_fl_base_d, (z.G + 1) * 4) &&
+             alloc(st, &sl.g_pl_list_d, (z.G + 1) * 4) && alloc(st, &sl.slot_of_row, cap1 * 4) &&
              alloc(st, &sl.row_of_slot, (z.n_slots_tok > 0 ? z.n_slots_tok : 1) * 4) &&
              alloc(st, &sl.h, cap1 * F * z.eb) &&
              alloc(st, &sl.y_perm, cap1 * D * 2);
@@ -462,8 +470,7 @@ static moe_status dispatch_impl(moe_stage *st, int32_t slot, const moe_microbatc
     a.blk_counts = sl.blk_counts;
     a.counts = sl.counts;
     a.offsets = sl.offsets;
-    a.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base,
-                          sl.g_fm_base, sl.g_fl_base, sl.g_pm_list, sl.g_pl_list};
+    a.groups = sl.tables();
     a.slot_of_row = sl.slot_of_row;
     a.row_of_slot = sl.row_of_slot;
     a.err = st->err;
@@ -517,10 +524,11 @@ static moe_status launch_ffn(moe_stage *st, GemmArgs &g1, GemmArgs &g2, int64_t 
         if (fp8) {
             e = launch_gemm_fp8(g2, false, mt, gmax, cus, cap, tmax, s);
         } else {
-            // the down product (K = f) keeps 256x256 tiles for every group:
-            // at ~130 rows its 28 column tiles per expert already fill the GPU
-            g2.large_all = 1;
-            e = launch_gemm_bf16(g2, false, mt, cus, s);
+            // the down product partitions the groups at kSmallRowsDown rows
+            GemmArgs g2d = g2;
+            g2d.groups = down_partition(g2.groups);
+            e = launch_gemm_bf16_small(g2d, false, gmax, cus, s);
+            if (e == hipSuccess) e = launch_gemm_bf16(g2d, false, mt, cus, s);
         }
     }
     if (e == hipErrorNotSupported) return MOE_EUNSUPPORTED;
@@ -559,8 +567,7 @@ static moe_status ffn_impl(moe_stage *st, int32_t slot, void *stream, bool rec)
     g1.N = 2 * d.d_ff;
     g1.K = d.d_model;
     g1.shared_group = d.has_shared_expert ? d.n_local_experts : -1;
-    g1.groups = GroupTable{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base,
-                          sl.g_fm_base, sl.g_fl_base, sl.g_pm_list, sl.g_pl_list};
+    g1.groups = sl.tables();
     g1.G = (int32_t)st->sz.G;
     g1.layer_id = sl.mb.layer_id;   // weights named on the device (NULL: layer 0)
     g1.layers = st->layers;
@@ -607,8 +614,7 @@ static moe_status ffn_grouped_impl(moe_stage *st, int32_t slot, const moe_groupe
     SlotWs &sl = st->slots[slot];
     sl.has_mb = false;               // nothing in this slot to combine
     if (n == 0) return record(sl, s);
-    const GroupTable gt{sl.g_row0, sl.g_rows, sl.g_mt_base, sl.g_lt_base, sl.g_st_base,
-                        sl.g_fm_base, sl.g_fl_base, sl.g_pm_list, sl.g_pl_list};
+    const GroupTable gt = sl.tables();
     {
         ProfScope ps(st, 0, s);
         if (launch_group_tables_from_counts(gb->counts, d.n_local_experts, n, gt, st->err, s) !=

@@ -263,18 +263,19 @@ def test_band_order_with_more_tiles_than_cus():
 def test_max_local_experts_and_group_size_boundaries():
     """256 local experts of 1024 (the largest tables the dispatch kernels
     size for, a shared expert making 257 groups) with crafted group sizes
-    around the small/large GEMM boundary: 1, 33, 160, 192 and 193 rows, and
-    many empty experts."""
+    around the small/large GEMM boundaries (gate/up at 192 rows, down at 64):
+    1, 33, 64, 65, 160, 192 and 193 rows, and many empty experts."""
     cfg = inputs.MoEConfig("maxE", d=256, f=128, E=1024, e0=512, E_loc=256, k=2, lengths=(0,),
                            has_shared=True, seed=8)
     rng = np.random.default_rng(8)
-    sizes = {512 + 0: 192, 512 + 1: 193, 512 + 2: 160, 512 + 3: 33, 512 + 4: 1}
+    sizes = {512 + 0: 192, 512 + 1: 193, 512 + 2: 160, 512 + 3: 33, 512 + 4: 1, 512 + 5: 64,
+             512 + 6: 65}
     first = np.concatenate([np.full(n, e, np.int32) for e, n in sizes.items()])
-    T = first.size                                       # 579 tokens
+    T = first.size                                       # 708 tokens
     rng.shuffle(first)
     # second choice: a non-local expert or a sparse spread over the other local experts
     second = np.where(rng.random(T) < 0.7, rng.integers(0, 512, T),
-                      rng.integers(512 + 5, 512 + 256, T)).astype(np.int32)
+                      rng.integers(512 + 7, 512 + 256, T)).astype(np.int32)
     ids = np.stack([first, second], 1)
     x = torch.randn((T, cfg.d), generator=torch.Generator("cuda").manual_seed(2),
                     device="cuda").to(torch.bfloat16)
@@ -285,11 +286,12 @@ def test_max_local_experts_and_group_size_boundaries():
 def test_partial_row_tiles_in_size_order():
     """The 256-row GEMM runs every group's full row tiles first and then the
     partial ones by decreasing size.  Group sizes around every tile boundary
-    (0, 1, 31..33, 128/129, 192/193, 255..257, 511..513), two groups with the
+    (0, 1, 31..33, 63..65, 128/129, 192/193, 255..257, 511..513), two groups with the
     same partial size (300 and 44 rows), a group with several full tiles
-    (700) and a shared expert over all 4387 tokens; outputs start as NaN, so a
+    (700) and a shared expert over all 4579 tokens; outputs start as NaN, so a
     tile that no workgroup ran fails the comparison."""
-    sizes = [0, 1, 31, 32, 33, 128, 129, 192, 193, 255, 256, 257, 300, 511, 512, 513, 700, 44]
+    sizes = [0, 1, 31, 32, 33, 63, 64, 65, 128, 129, 192, 193, 255, 256, 257, 300, 511, 512, 513,
+             700, 44]
     cfg = inputs.MoEConfig("tile_order", d=256, f=128, E=24, e0=0, E_loc=len(sizes), k=1,
                            lengths=(0,), has_shared=True, seed=12)
     rng = np.random.default_rng(12)
