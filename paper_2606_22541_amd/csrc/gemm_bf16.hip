@@ -84,6 +84,17 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, in
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, n, 0x00020000);
 }
 
+// Tile Lg of a group with Mt row tiles and NT column tiles, in bands of up
+// to kBandM row tiles (row tiles fastest within a band).
+__device__ __forceinline__ void band_tile(int Lg, int Mt, int NT, int &mt, int &nt)
+{
+    const int band = Lg / (kBandM * NT);
+    const int r = Lg - band * kBandM * NT;
+    const int bm = min(kBandM, Mt - band * kBandM);
+    mt = band * kBandM + r % bm;
+    nt = r / bm;
+}
+
 __device__ __forceinline__ void decode_tile(int L, const int32_t *__restrict__ tbase, int G,
                                             int NT, int &g, int &mt, int &nt)
 {
@@ -93,13 +104,7 @@ __device__ __forceinline__ void decode_tile(int L, const int32_t *__restrict__ t
         if (tbase[mid] * NT <= L) lo = mid; else hi = mid;
     }
     g = lo;
-    const int Lg = L - tbase[g] * NT;
-    const int Mt = tbase[g + 1] - tbase[g];
-    const int band = Lg / (kBandM * NT);
-    const int r = Lg - band * kBandM * NT;
-    const int bm = min(kBandM, Mt - band * kBandM);
-    mt = band * kBandM + r % bm;
-    nt = r / bm;
+    band_tile(L - tbase[g] * NT, tbase[g + 1] - tbase[g], NT, mt, nt);
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -454,22 +459,48 @@ void k_gemm_bf16(GemmArgs a)
     w.a_rd = (wm * 128 + rd_row) * kRowElems;
     w.b_rd = (wn * 2) * 2 * 512 + lane * 8;
 
+    // The group tables in one round trip for the whole launch: with G < 64
+    // groups, lane i holds the tile prefix at i (i <= G), rows[i] and
+    // row0[i] (i < G), and a tile's group is found by a ballot instead of a
+    // binary search of dependent loads per tile.
+    const int G = a.G;
+    const bool few = G < 64;
+    const int32_t *obase = by_size ? fbase : tbase;   // the order's full-tile prefix
+    int ob_l = 0, rows_l = 0, row0_l = 0;
+    if (few) {
+        const int gi = min(lane, G - 1);
+        ob_l = obase[min(lane, G)];
+        rows_l = a.groups.rows[gi];
+        row0_l = a.groups.row0[gi];
+    }
+
     for (int L = first; L < total; L += P) {
         int g, mt, nt;
         if (L < n_full) {
-            decode_tile(L, by_size ? fbase : tbase, a.G, NT, g, mt, nt);
+            if (few) {
+                // largest g < G with obase[g] * NT <= L (obase is nondecreasing, obase[0] = 0)
+                g = __builtin_popcountll(__ballot(lane < G && ob_l * NT <= L)) - 1;
+                g = __builtin_amdgcn_readfirstlane(g);
+                const int b0 = __builtin_amdgcn_readlane(ob_l, g);
+                const int b1 = __builtin_amdgcn_readlane(ob_l, g + 1);
+                band_tile(L - b0 * NT, b1 - b0, NT, mt, nt);
+            } else {
+                decode_tile(L, obase, G, NT, g, mt, nt);
+            }
         } else {
             // partial row tiles, largest first; a group's column tiles are consecutive
             const int j = (L - n_full) / NT;
             nt = L - n_full - j * NT;
-            g = plist[j];
-            mt = a.groups.rows[g] / kBM;
+            g = __builtin_amdgcn_readfirstlane(plist[j]);
+            mt = (few ? __builtin_amdgcn_readlane(rows_l, g) : a.groups.rows[g]) / kBM;
         }
         g = __builtin_amdgcn_readfirstlane(g);
         mt = __builtin_amdgcn_readfirstlane(mt);
         nt = __builtin_amdgcn_readfirstlane(nt);
-        const int grows = __builtin_amdgcn_readfirstlane(a.groups.rows[g]);
-        const int row0 = __builtin_amdgcn_readfirstlane(a.groups.row0[g]) + mt * kBM;
+        const int grows = __builtin_amdgcn_readfirstlane(
+            few ? __builtin_amdgcn_readlane(rows_l, g) : a.groups.rows[g]);
+        const int row0 = __builtin_amdgcn_readfirstlane(
+            few ? __builtin_amdgcn_readlane(row0_l, g) : a.groups.row0[g]) + mt * kBM;
         const int rows_valid = min(kBM, grows - mt * kBM);
         const int n0 = nt * kBN;
         const bool sh = (g == a.shared_group);
