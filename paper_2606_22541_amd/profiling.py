@@ -30,7 +30,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = {
     "gemm_gate_up_swiglu": ["csrc/gemm_bf16.hip", "csrc/gemm_bf16_small.hip", "csrc/common.h",
                             "csrc/kernels.h"],
-    "gemm_down": ["csrc/gemm_bf16.hip", "csrc/common.h", "csrc/kernels.h"],
+    "gemm_down": ["csrc/gemm_bf16.hip", "csrc/gemm_bf16_small.hip", "csrc/common.h",
+                  "csrc/kernels.h"],
     "gemm_gate_up_swiglu_fp8": ["csrc/gemm_fp8.hip", "csrc/common.h", "csrc/kernels.h"],
     "gemm_down_fp8": ["csrc/gemm_fp8.hip", "csrc/common.h", "csrc/kernels.h"],
     "combine": ["csrc/combine.hip", "csrc/common.h", "csrc/kernels.h"],
@@ -44,10 +45,12 @@ NAME_MAP = (
     ("void moe::k_gemm_bf16_small<true>", "gemm_gate_up_swiglu"),
     ("void moe::k_gemm_bf16<true>", "gemm_gate_up_swiglu"),
     ("void moe::k_gemm_bf16<false>", "gemm_down"),
+    ("void moe::k_gemm_bf16_small<false>", "gemm_down"),
     ("void moe::k_gemm_fp8<true>", "gemm_gate_up_swiglu_fp8"),
     ("void moe::k_gemm_fp8<false>", "gemm_down_fp8"),
     ("moe::k_combine", "combine"),
     ("moe::k_gather_scales", "gather"),
+    ("moe::k_transpose_scales", "gather"),
     ("moe::k_hist", "dispatch_index"),
     ("moe::k_place", "dispatch_index"),
     ("moe::k_quantize_fp8", "quantize_fp8"),
