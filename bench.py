@@ -72,9 +72,12 @@ def stream_accounting(cfg, counts_local, n_tokens_with_local, T):
     # the gather runs in fp8 mode only and moves the token scales (one fp32
     # per 128 channels; the GEMM reads the e4m3 rows of x itself): each
     # token's scales read once, one row of scales written per routed row,
-    # plus slot_of_row
+    # plus slot_of_row (and, with a shared expert, every token's scales
+    # transposed for it)
     sb = (d // 128) * 4
     gather = n_tokens_with_local * sb + n_loc * sb + n_loc * 4
+    if cfg.has_shared:
+        gather += 2 * T * sb     # the shared expert's scales, transposed for all T rows
     combine = T * k * 12 + n_loc * rb + T * rb + (T * rb if cfg.has_shared else 0)
     return dict(index_bytes=index, gather_bytes=gather, combine_bytes=combine)
 
