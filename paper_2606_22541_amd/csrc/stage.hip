@@ -32,8 +32,7 @@ struct SlotWs {
                           g_pl_list, g_lt_base_d, g_st_base_d, g_fl_base_d, g_pl_list_d};
     }
     int32_t *slot_of_row = nullptr, *row_of_slot = nullptr;
-    void *x_perm = nullptr;
-    float *x_perm_s = nullptr;
+    float *x_perm_s = nullptr;     // fp8: the routed rows' x scales, transposed
     void *h = nullptr;
     float *h_s = nullptr;
     void *y_perm = nullptr;
@@ -786,7 +785,7 @@ moe_status moe_stage_query(moe_stage *st, int32_t slot, moe_dispatch_view *v)
     v->offsets = sl.offsets;
     v->slot_of_row = sl.slot_of_row;
     v->row_of_slot = sl.row_of_slot;
-    v->x_perm = sl.x_perm;
+    v->x_perm = nullptr;              // the row gather is part of the gate/up GEMM
     v->x_perm_scales = sl.x_perm_s;
     v->h = sl.h;
     v->h_scales = sl.h_s;
