@@ -28,8 +28,10 @@
 //  * token rows are 64 bytes per step in LDS, their 16-byte chunks
 //    XOR-swizzled by (row / 4) % 4 so that the 16-lane groups of each
 //    ds_read_b128 hit 64 distinct banks; weight fragments arrive in MFMA
-//    fragment order (see launch_pack_frag_bf16), one contiguous 1 KB per
-//    load, and are read back lane-contiguous, also free of bank conflicts;
+//    fragment order, one contiguous 1 KB per load, a tile's 16 fragments of
+//    a step being one contiguous 16 KB run of the panel-ordered weights
+//    (see launch_pack_frag_bf16), and are read back lane-contiguous, also
+//    free of bank conflicts;
 //  * every step of a wave issues the same loads (steps past K re-read the
 //    last one), so the wait before each step is a constant and no wait
 //    drains the look-ahead;
@@ -113,12 +115,12 @@ struct Tile {
     __amdgpu_buffer_rsrc_t ra, rb;
     int KT;
     int ncb;           // weight column blocks present in the tile (8, or fewer at N's end)
+    int stepb;         // bytes of one K step of the tile's weight panel (ncb x 2 KB)
     int va0, va1;      // token fills: offsets of rows 32 w + lane / 4 (+16), swizzled chunk
 };
 
 struct WaveConst {
     int voff_b;        // weight fill: lane * 16
-    int cbstride;      // bytes between weight column blocks
     int a_rd;          // LDS element offset of this lane's token row (block 0)
     int b_rd;          // LDS element offset of this lane's weight fragment (block 0)
     int wave, rd_hi, swz;
@@ -152,7 +154,7 @@ __device__ __forceinline__ void fill_one(const Tile &t, const WaveConst &w, cons
         const int cb = min(f >> 1, t.ncb - 1), kk = f & 1;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
             t.rb, (lds_void *)(st.b + f * 512), 16, w.voff_b,
-            cb * w.cbstride + (js * 2 + kk) * 1024, 0, STREAM ? kNonTemporal : 0);
+            js * t.stepb + (cb * 2 + kk) * 1024, 0, STREAM ? kNonTemporal : 0);
     }
 }
 
@@ -452,7 +454,6 @@ void k_gemm_bf16(GemmArgs a)
     const int frow = w.wave * 32 + (lane >> 2);
     const int fchunk = ((lane & 3) ^ ((lane >> 4) & 3)) << 4;
     w.voff_b = lane * 16;
-    w.cbstride = (K / 16) * 1024;
     const int rd_row = lane & 31;
     w.rd_hi = lane >> 5;
     w.swz = (rd_row >> 2) & 3;
@@ -524,6 +525,7 @@ void k_gemm_bf16(GemmArgs a)
         t.rb = make_rsrc(B, (int64_t)min(kBN, N - n0) * K * 2);
         t.KT = K / kBK;
         t.ncb = min(kBN, N - n0) / 32;
+        t.stepb = t.ncb * 2048;
 
         // 32-row blocks of this wave's 128-row half that hold rows (uniform per
         // wave); in band order every tile runs all of them

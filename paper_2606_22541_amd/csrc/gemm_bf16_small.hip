@@ -14,7 +14,9 @@
 //    once per tile;
 //  * weights go straight from HBM into a 4-deep register ring (each wave
 //    loads only its own columns and K half: four 1 KB fragments per step,
-//    each a contiguous load thanks to the fragment-order weight layout);
+//    each a contiguous load thanks to the fragment layout, and the four
+//    waves' loads of a step together two contiguous 8 KB runs of the
+//    panel-ordered weights);
 //    they are read once, so the loads are non-temporal and the stream does
 //    not displace the activations other kernels read next, nor force out
 //    the dirty lines of earlier ones while it runs; so
@@ -82,18 +84,17 @@ struct SmallTile {
     bf16 *C;
     int row0, rows_valid, n0, N, K, KT;
     int avoff[6];      // token-row load offsets of this lane's row blocks wave + 4 i
+    int vb;            // this lane's weight load offset in the 256-column panel (K step 0)
+    int sstep;         // bytes of the panel per 64-wide K step
 };
 
 struct SmallLds {
     bf16 *a[kRing];   // token-row tiles, 192 rows x 64 bf16 each
 };
 
-// Per-wave constants: which K half and column half the wave owns, and the
-// lane's weight-load offsets.
+// Per-wave constants: which K half and column half the wave owns.
 struct SmallWave {
     int wave, lane, kh, ch;
-    int vb;                    // weight fragment (column block 2 ch, sub-step 2 kh)
-    int cbstride;              // bytes between column blocks
 };
 
 // Fills of step j: token rows into a[I] (direct to LDS), weights into the
@@ -112,11 +113,11 @@ __device__ __forceinline__ void fill_step(const SmallTile &t, const SmallLds &l,
             t.ra, (lds_void_s *)(l.a[I] + (w.wave + 4 * i) * 8 * kRowEs), 16, t.avoff[i],
             js * kBKs * 2, 0, 0);
     // [column block][sub-step]: q = 2 cb + m holds sub-step 2 kh + m
-    const int soff = js * 4 * 1024;
-    breg[I][0] = load_b128(t.rb, w.vb, soff);
-    breg[I][1] = load_b128(t.rb, w.vb + 1024, soff);
-    breg[I][2] = load_b128(t.rb, w.vb + w.cbstride, soff);
-    breg[I][3] = load_b128(t.rb, w.vb + w.cbstride + 1024, soff);
+    const int soff = js * t.sstep;
+    breg[I][0] = load_b128(t.rb, t.vb, soff);
+    breg[I][1] = load_b128(t.rb, t.vb + 1024, soff);
+    breg[I][2] = load_b128(t.rb, t.vb + 2048, soff);
+    breg[I][3] = load_b128(t.rb, t.vb + 3072, soff);
 }
 
 // Inside the K loop the same loads are split: the step's four weight loads
@@ -130,11 +131,11 @@ __device__ __forceinline__ void fill_weights(const SmallTile &t, const SmallWave
                                              bf16x8 (&breg)[kRing][4])
 {
     const int js = min(j, t.KT - 1);
-    const int soff = js * 4 * 1024;
-    breg[I][0] = load_b128(t.rb, w.vb, soff);
-    breg[I][1] = load_b128(t.rb, w.vb + 1024, soff);
-    breg[I][2] = load_b128(t.rb, w.vb + w.cbstride, soff);
-    breg[I][3] = load_b128(t.rb, w.vb + w.cbstride + 1024, soff);
+    const int soff = js * t.sstep;
+    breg[I][0] = load_b128(t.rb, t.vb, soff);
+    breg[I][1] = load_b128(t.rb, t.vb + 1024, soff);
+    breg[I][2] = load_b128(t.rb, t.vb + 2048, soff);
+    breg[I][3] = load_b128(t.rb, t.vb + 3072, soff);
 }
 
 template <int I>
@@ -333,10 +334,6 @@ void k_gemm_bf16_small(GemmArgs a)
     const float *Bsw;
     resolve_weights(a, Bw, Bsw);
 
-    // fragment-order weights: column block cb of the tile starts at
-    // cb * cbstride, sub-step kk of a step at kk KB
-    w.cbstride = (K / 16) * 1024;
-    w.vb = 2 * w.ch * w.cbstride + 2 * w.kh * 1024 + w.lane * 16;
 
     for (int L = first; L < total; L += P) {
         // tile L: j-th small group, column block nt (an expert's column
@@ -369,14 +366,22 @@ void k_gemm_bf16_small(GemmArgs a)
         const bool indexed = a.A_index != nullptr && !sh;
         const bf16 *A = indexed ? (const bf16 *)a.A_routed
                                 : (const bf16 *)(sh ? a.A_shared : a.A_routed) + (int64_t)t.row0 * K;
-        const bf16 *B = (const bf16 *)Bw + ((int64_t)g * N + t.n0) * K;
+        // panel-order weights: the tile is one half of a 256-column panel,
+        // which holds per 32-wide K step its ncb column blocks' two 1 KB
+        // fragments contiguously; wave (kh, ch) reads column blocks
+        // 4 half + 2 ch and + 1 of the panel's K step 2 js + kh
+        const int p0 = t.n0 & ~255, half = (t.n0 >> 7) & 1;
+        const int ncb = min(8, (N - p0) / 32);
+        const bf16 *B = (const bf16 *)Bw + ((int64_t)g * N + p0) * K;
+        t.sstep = ncb * 4096;
+        t.vb = w.kh * ncb * 2048 + (4 * half + 2 * w.ch) * 2048 + w.lane * 16;
         t.ra = rsrc_s(A, (indexed ? a.A_routed_rows : (int64_t)t.rows_valid) * K * 2);
 #pragma unroll
         for (int i = 0; i < 6; ++i)
             t.avoff[i] = token_row_offset(indexed ? a.A_index : nullptr, a.A_index_div, t.row0,
                                           8 * (w.wave + 4 * i) + (w.lane >> 3), t.rows_valid,
                                           K * 2, w.lane);
-        t.rb = rsrc_s(B, (int64_t)min(kTNs, N - t.n0) * K * 2);
+        t.rb = rsrc_s(B, (int64_t)ncb * 32 * K * 2);
         t.C = (bf16 *)(sh ? a.C_shared : a.C_routed);
         switch ((t.rows_valid + 31) >> 5) {   // 32-row blocks holding rows: 1..6
         case 1: run_small_tile<SWIGLU, 1>(t, l, w); break;

@@ -174,10 +174,14 @@ hipError_t launch_ingest_signal(uint32_t *word, uint32_t epoch, hipStream_t s);
 // all within one 128-row scale block of each.
 constexpr int kInterleaveBf16 = 16;
 constexpr int kInterleaveFp8 = 16;
-// bf16 weights in MFMA fragment order (the layout both bf16 grouped-GEMM
-// kernels read B in): chunk ((m * N/32 + n/32) * K/16 + k/16) * 64 + n % 32 +
-// 32 ((k/8) % 2) of 16 bytes holds row n, columns k..k+7 (k % 8 == 0).  With
-// `up` non-null the packed rows interleave gate and up by `interleave`.
+// bf16 weights in MFMA fragments, panel order (the layout both bf16
+// grouped-GEMM kernels read B in).  The 1 KB fragment of 32-column block b and
+// 16-wide K sub-step u holds, in 16-byte chunk n % 32 + 32 ((k/8) % 2), row
+// n, columns k..k+7 (k % 8 == 0).  Fragments are grouped in panels of 256
+// columns (8 blocks; fewer at N's end): a panel stores, for each 32-wide K
+// step s, its blocks' fragments (b, 2s) and (b, 2s + 1) contiguously, block
+// by block, so one K step of a panel is a single contiguous run.  With `up`
+// non-null the packed rows interleave gate and up by `interleave`.
 hipError_t launch_pack_frag_bf16(const void *gate, const void *up, void *dst, int32_t n_mats,
                                  int32_t N, int32_t K, int32_t interleave, hipStream_t s);
 // e4m3 weights in the fragment order of the 16x16x128 f8 MFMA: chunk

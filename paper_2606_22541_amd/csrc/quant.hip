@@ -134,13 +134,16 @@ hipError_t launch_pack_frag_fp8(const void *gate, const void *up, void *dst, int
     return hipGetLastError();
 }
 
-// bf16 weights in MFMA fragment order.  Row n (of N) and column k (of K) of
-// matrix m go to 16-byte chunk ((m * N/32 + n/32) * K/16 + k/16) * 64 + lane,
-// element k % 8, with lane = n % 32 + 32 * ((k / 8) % 2): the 64 lanes'
-// operands of one 32-column x 16-K B fragment of v_mfma_f32_32x32x16_bf16
-// are 1 KB of consecutive memory, and a column block's fragments follow
-// each other along K.  With `up` given, packed row n interleaves gate and up
-// rows in blocks of `il` (N = 2 f rows per matrix).
+// bf16 weights in MFMA fragments, panel order.  Row n (of N) and column k
+// (of K) of matrix m go to chunk `lane` = n % 32 + 32 ((k / 8) % 2) of the
+// fragment of column block n / 32 and K sub-step k / 16, element k % 8: the 64
+// lanes' operands of one 32-column x 16-K B fragment of
+// v_mfma_f32_32x32x16_bf16 are 1 KB of consecutive memory.  Blocks form
+// panels of 8 (256 columns; the last panel may hold fewer), and a panel
+// stores each 32-wide K step's fragments together ([K step][block][sub-step]),
+// so a GEMM tile's weights for one K step are one contiguous run.  With `up`
+// given, packed row n interleaves gate and up rows in blocks of `il` (N = 2 f
+// rows per matrix).
 __global__ void k_pack_frag_bf16(const uint4 *__restrict__ gate, const uint4 *__restrict__ up,
                                  uint4 *__restrict__ dst, int32_t n_mats, int32_t N, int32_t K,
                                  int32_t il)
@@ -165,7 +168,13 @@ __global__ void k_pack_frag_bf16(const uint4 *__restrict__ gate, const uint4 *__
             src = (i < il) ? gate : up;
             srow = b * il + (i % il);
         }
-        dst[q] = src[((int64_t)m * rows_per_src + srow) * row_vecs + kv];
+        // panel order: 256-column tile t = nb / 8 holds, per 32-wide K step,
+        // its column blocks' two 1 KB fragments contiguously
+        const int t = nb >> 3, lb = nb & 7, ncb = min(8, nbs - 8 * t);
+        const int64_t off = ((int64_t)m * nbs + 8 * t) * (int64_t)kc * 64       // tiles before
+                            + (int64_t)(kk >> 1) * ncb * 128                     // K steps before
+                            + (lb * 2 + (kk & 1)) * 64 + lane;
+        dst[off] = src[((int64_t)m * rows_per_src + srow) * row_vecs + kv];
     }
 }
 
