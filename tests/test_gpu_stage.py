@@ -51,6 +51,8 @@ def test_c0_tiny_full_parity():
 @pytest.mark.parametrize("T,d,f,E,E_loc,k", [
     (700, 1024, 384, 16, 4, 4),     # several row and column tiles, ragged tails
     (333, 640, 256, 8, 3, 2),       # d = 640: partial 256-column tile in the down GEMM
+    (100, 640, 256, 8, 3, 2),       # groups of <= 64 rows: the down GEMM's small-group tiles end
+                                    # in a half weight panel (d = 640 = 2.5 panels of 256)
     (1, 256, 128, 8, 4, 2),         # one token
     (257, 256, 128, 1, 1, 1),       # one expert, 257 rows: tile + 1
 ])
