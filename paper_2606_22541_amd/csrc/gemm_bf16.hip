@@ -2,7 +2,8 @@
 // the left, one expert's weights on the right; section 3.4.2).
 //
 // C[g] = A[g] * B[g]^T for every group g (a local expert, or the shared
-// expert), where A[g] is a run of rows of X_perm (or H), K-contiguous, and
+// expert), where A[g] is a run of token rows (gathered from x through
+// slot_of_row) or of H, K-contiguous, and
 // B[g] is the expert's [N][K] weight matrix stored in MFMA fragment order
 // (see launch_pack_frag_bf16).
 //

@@ -56,7 +56,7 @@ struct LayerWeights {
 };
 
 struct GemmArgs {
-    const void *A_routed;    // [rows][K] (rows of X_perm or H), or x itself when A_index is set
+    const void *A_routed;    // [rows][K] (rows of H, or pre-grouped rows), or x itself when A_index is set
     const void *A_shared;    // [T][K] (x or H_shared) for group E_loc, if shared
     const float *As_routed;  // fp8: [rows][K/128] scales of A
     const float *As_shared;

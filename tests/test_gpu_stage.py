@@ -1,6 +1,6 @@
 """GPU parity of the HIP expert stage against the CPU oracle (bf16 path).
 
-Bit-exact: counts, offsets, slot_of_row, row_of_slot (X_perm is not materialised in bf16:
+Bit-exact: counts, offsets, slot_of_row, row_of_slot (X_perm is not materialised:
 the gate/up GEMM gathers the token rows itself, so the gather is checked through the outputs).
 Floating point: rel-L2 <= 1e-2 on outputs and per expert on Y_perm rows.
 """
