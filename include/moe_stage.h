@@ -336,8 +336,8 @@ MOE_API moe_status moe_stage_sync(moe_stage *stage);
  * While enabled, every enqueue call records an event pair around each of its
  * kernel groups on the launch stream (this creates events, i.e. allocates
  * host-side runtime objects).  Kinds, in order: 0 dispatch index
- * (histogram, scan, scatter), 1 row gather (fp8 only; in bf16 it is part of
- * kind 2), 2 grouped GEMM gate/up with the SiLU*up epilogue (fp8: and the
+ * (histogram, scan, scatter), 1 gather of the token scales (fp8 only; the
+ * rows themselves are gathered inside kind 2), 2 grouped GEMM gate/up with the SiLU*up epilogue (fp8: and the
  * quantisation of h), 3 grouped GEMM down, 4 combine, 5 reserved (no
  * longer recorded). */
 #define MOE_PROF_KINDS 6
