@@ -341,6 +341,68 @@ def describe(r):
         per=r["n_local_slots"] // c.E_loc)
 
 
+def secondary_result(name, steps, warmup):
+    """One further workload's entry of the JSON line."""
+    sec = run_workload(name, steps, warmup)
+    out = {
+        "workload": describe(sec),
+        "tokens_per_step": sec["T"],
+        "tokens_per_s": round(sec["T"] * sec["steps"] / (sec["ms"] / 1e3), 1),
+        "ms_per_step": round(sec["ms"] / sec["steps"], 4),
+        "spread_ms_per_step": sec["spread"],
+    }
+    if sec["n_micro"] > 1:
+        # overlapping streams: the roofline is the step's; kernel rates
+        # come from a pass with the micro-batches one after another
+        out["roofline"] = step_roofline(sec)
+        out["kernels_serialized"] = stream_rooflines(sec)
+        out["hw_queues"] = os.environ.get("GPU_MAX_HW_QUEUES", "runtime default")
+    else:
+        out["roofline"] = roofline_for(sec)
+        out["kernels"] = stream_rooflines(sec)
+    return out
+
+
+# The HIP runtime maps a process's streams onto GPU_MAX_HW_QUEUES hardware
+# queues (4 unless set), and two streams on one queue run one after the other.
+# With 4 queues the four streams of a multi-micro-batch workload (c2, c4) share
+# queues in a fresh process (c2 1.31 ms, c4 0.712 ms a step); with 8 they get
+# one each (1.10 and 0.615 ms on the same box).  Such workloads are measured
+# in a process started with MULTI_STREAM_QUEUES queues; single-stream ones keep
+# the environment's setting (with 32 queues, single-stream timings showed
+# stalls of a few hundred microseconds).
+MULTI_STREAM_QUEUES = 8
+
+
+def multi_stream(name):
+    """True when the workload runs several micro-batches on streams of their own."""
+    from paper_2606_22541_amd import inputs
+    c = inputs.CONFIGS[name]
+    return (len(c.lengths) if c.lengths is not None else c.n_micro) > 1
+# GPU_MAX_HW_QUEUES as the process found it
+_ENV_HW_QUEUES = os.environ.get("GPU_MAX_HW_QUEUES")
+
+
+def _env_with_queues(n):
+    env = dict(os.environ)
+    if n is None:
+        env.pop("GPU_MAX_HW_QUEUES", None)
+    else:
+        env["GPU_MAX_HW_QUEUES"] = str(n)
+    return env
+
+
+def run_secondary_child(name, steps, warmup, queues):
+    """A multi-stream workload in a fresh process with `queues` hardware queues."""
+    r = subprocess.run([sys.executable, os.path.abspath(__file__), "--workload-child", name,
+                        "--steps", str(steps), "--warmup", str(warmup),
+                        "--multi-stream-queues", str(queues)],
+                       capture_output=True, text=True, timeout=600, env=_env_with_queues(queues))
+    if r.returncode != 0:
+        raise RuntimeError("workload %s child failed: %s" % (name, r.stderr.strip()[-2000:]))
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
 def run_pipelined(name="c1", n_streams=3, steps=40, warmup=30, repeats=3):
     """Throughput of a stream of micro-batches of workload `name` with up to
     n_streams of them in flight: micro-batch i is submitted on stream
@@ -564,8 +626,11 @@ def run_cu_partition(name="c1", partitions=("all_cus", "split16", "split32", "ge
     of its own (a fresh budget of hardware queues)."""
     res = []
     for part in partitions:
+        # the children keep the environment's hardware-queue count (each
+        # masked stream takes a queue of its own; the layouts were measured so)
         r = subprocess.run([sys.executable, os.path.abspath(__file__), "--cu-partition-child", part,
-                            "--workload", name], capture_output=True, text=True, timeout=300)
+                            "--workload", name, "--multi-stream-queues", "0"], capture_output=True,
+                           text=True, timeout=300, env=_env_with_queues(_ENV_HW_QUEUES))
         if r.returncode != 0:
             res.append({"partition": part, "error": r.stderr.strip().splitlines()[-1:]})
             continue
@@ -974,6 +1039,11 @@ def main():
                     help="also time the three-stream layout on CU-masked streams (0: skip)")
     ap.add_argument("--cu-partition-child", default="",
                     help="internal: measure one CU partition in this (fresh) process and exit")
+    ap.add_argument("--multi-stream-queues", type=int, default=MULTI_STREAM_QUEUES,
+                    help="hardware queues (GPU_MAX_HW_QUEUES) of the processes that measure "
+                         "multi-micro-batch workloads (0: the environment's, in this process)")
+    ap.add_argument("--workload-child", default="",
+                    help="internal: measure this workload in this (fresh) process and exit")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -982,9 +1052,15 @@ def main():
               "across GPUs the stage shards by expert, one process per GPU on its own experts."
               % args.gpus, file=sys.stderr)
         sys.exit(2)
+    if args.multi_stream_queues > 0 and multi_stream(args.workload_child or args.workload):
+        # set before HIP starts (the first CUDA call below)
+        os.environ["GPU_MAX_HW_QUEUES"] = str(args.multi_stream_queues)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.workload_child:
+        print(json.dumps(secondary_result(args.workload_child, args.steps, args.warmup)), flush=True)
+        return
     if args.cu_partition_child:
         print(json.dumps(run_cu_partition_child(args.cu_partition_child, args.workload)), flush=True)
         return
@@ -1028,22 +1104,11 @@ def main():
         line["%s_ingest" % args.workload] = run_ingest(args.workload)
         _log("[bench] ingest %s done" % args.workload)
     for name in [n for n in args.secondary.split(",") if n]:
-        sec = run_workload(name, max(args.steps // 2, 5), args.warmup)
-        line[name] = {
-            "workload": describe(sec),
-            "tokens_per_step": sec["T"],
-            "tokens_per_s": round(sec["T"] * sec["steps"] / (sec["ms"] / 1e3), 1),
-            "ms_per_step": round(sec["ms"] / sec["steps"], 4),
-            "spread_ms_per_step": sec["spread"],
-        }
-        if sec["n_micro"] > 1:
-            # overlapping streams: the roofline is the step's; kernel rates
-            # come from a pass with the micro-batches one after another
-            line[name]["roofline"] = step_roofline(sec)
-            line[name]["kernels_serialized"] = stream_rooflines(sec)
+        steps = max(args.steps // 2, 5)
+        if args.multi_stream_queues > 0 and multi_stream(name):
+            line[name] = run_secondary_child(name, steps, args.warmup, args.multi_stream_queues)
         else:
-            line[name]["roofline"] = roofline_for(sec)
-            line[name]["kernels"] = stream_rooflines(sec)
+            line[name] = secondary_result(name, steps, args.warmup)
         _log("[bench] %s done" % name)
     if args.pipelined_streams > 1:
         line["%s_pipelined" % args.workload] = run_pipelined(args.workload, args.pipelined_streams)
