@@ -113,6 +113,40 @@ def test_bad_expert_id_is_reported_and_skipped():
         assert np.array_equal(view["counts"], ref["counts"])
 
 
+@pytest.mark.parametrize("T", [1000, 4200])
+def test_bad_ids_in_many_dispatch_chunks(T):
+    """Bad ids spread over 8 and 33 chunks of 1024 slots (8000 and 33600
+    slots): reported once, placed as masked."""
+    cfg = inputs.MoEConfig("bad2", d=256, f=128, E=64, e0=8, E_loc=8, k=8, lengths=(T,), seed=14)
+    w = inputs.make_weights(cfg, "cuda")
+    rng = np.random.default_rng(14)
+    ids = rng.integers(-1, 64, size=(T, 8)).astype(np.int32)
+    bad = rng.choice(T * 8, size=5, replace=False)
+    ids.reshape(-1)[bad] = np.array([64, 100, -2, -50, 1 << 20], np.int32)
+    mb = inputs.MicroBatch(x=torch.ones((T, 256), dtype=torch.bfloat16, device="cuda"), ids=ids,
+                           w=np.full((T, 8), 0.125, np.float32))
+    with ExpertStage(cfg, w, max_tokens=T) as st:
+        i, wt = to_device_routing(ids, mb.w)
+        out = torch.zeros((T, 256), dtype=torch.bfloat16, device="cuda")
+        st.submit(st.microbatch(mb.x, i, wt, out))
+        assert C.moe_stage_sync_status(st.handle) == C.MOE_EBADID
+        assert C.moe_stage_sync_status(st.handle) == C.MOE_OK
+        view = st.view(0)
+        ref = oracle.dispatch(np.where((ids >= -1) & (ids < 64), ids, -1), 64, 8, 8)
+        assert np.array_equal(view["row_of_slot"], ref["row_of_slot"])
+        assert np.array_equal(view["counts"], ref["counts"])
+        assert np.array_equal(view["offsets"], ref["offsets"])
+
+
+@pytest.mark.parametrize("T,k,E,e0,E_loc", [
+    (4097, 8, 64, 8, 8),          # 32776 slots: a last chunk of 8 slots
+    (16385, 2, 1024, 512, 256),   # 32770 slots over 1024 experts, 256 of them local
+])
+def test_dispatch_many_chunks_and_largest_tables(T, k, E, e0, E_loc):
+    cfg = inputs.MoEConfig("cnt", d=256, f=128, E=E, e0=e0, E_loc=E_loc, k=k, lengths=(T,), seed=13)
+    _case(cfg)
+
+
 def test_host_errors_enqueue_nothing():
     cfg = inputs.MoEConfig("err", d=256, f=128, E=8, e0=0, E_loc=4, k=2, lengths=(4,), seed=7)
     w = inputs.make_weights(cfg, "cuda")
