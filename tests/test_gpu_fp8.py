@@ -40,13 +40,14 @@ def test_quantizer_bit_exact(T, d, scale):
         list(zip(*bad))[:5], got_q[bad][:5], codes[bad][:5])
 
 
-def _case(cfg, *, n_streams=1):
+def _case(cfg, mbs=None, *, n_streams=1):
     """Every token and every Y_perm row against the oracle, with the
     workspace poisoned with NaN before the run."""
     log("fp8 case %s: d=%d f=%d E=%d E_loc=%d k=%d lengths=%s shared=%d streams=%d" % (
         cfg.name, cfg.d, cfg.f, cfg.E, cfg.E_loc, cfg.k, cfg.lengths, cfg.has_shared, n_streams))
     w = inputs.make_weights(cfg, "cuda")
-    mbs = inputs.make_microbatches(cfg, "cuda")
+    if mbs is None:
+        mbs = inputs.make_microbatches(cfg, "cuda")
     ow = CachedWeights(oracle.OracleWeights(w, "fp8"))
     streams = [torch.cuda.Stream() for _ in range(n_streams)] if n_streams > 1 else None
     Tmax = max(max(mb.ids.shape[0] for mb in mbs), 1)
@@ -92,3 +93,47 @@ def test_fp8_many_row_tiles_per_group():
     routed rows; every row is checked."""
     _case(inputs.MoEConfig("f8band", d=1024, f=512, E=16, e0=0, E_loc=8, k=8, lengths=(6500,),
                            dtype="fp8", seed=21))
+
+
+def test_fp8_edge_cases():
+    """Crafted routings around the fp8 kernel's 128-token tiles: one token,
+    all slots masked, one expert taking both slots of 300 tokens (600 rows),
+    127 / 128 / 129 rows on one expert, and a mixed routing with masks."""
+    cfg = inputs.MoEConfig("f8edge", d=256, f=128, E=8, e0=0, E_loc=4, k=2, lengths=(0,),
+                           dtype="fp8", seed=15)
+    rng = np.random.default_rng(15)
+
+    def rows_on(e, n, T):
+        ids = np.full((T, 2), -1, np.int32)
+        ids[:n, 0] = e
+        ids[n:, 0] = rng.integers(4, 8, T - n)          # the rest go to non-local experts
+        return ids
+
+    cases = {
+        "one_token": np.array([[1, 3]], np.int32),
+        "all_masked": np.full((9, 2), -1, np.int32),
+        "one_expert_both_slots": np.full((300, 2), 2, np.int32),
+        "tile_minus_one": rows_on(1, 127, 200),
+        "tile": rows_on(1, 128, 200),
+        "tile_plus_one": rows_on(3, 129, 200),
+        "mixed": rng.integers(-1, 8, size=(513, 2)).astype(np.int32),
+    }
+    for name, ids in cases.items():
+        T = ids.shape[0]
+        log("fp8 edge case %s T=%d" % (name, T))
+        x = (torch.randn((T, cfg.d), generator=torch.Generator("cuda").manual_seed(T),
+                         device="cuda")).to(torch.bfloat16)
+        mb = inputs.MicroBatch(x=x, ids=ids, w=rng.random((T, 2)).astype(np.float32))
+        _case(inputs.scaled(cfg, name="f8edge_" + name, lengths=(T,)), [mb])
+
+
+def test_c1p_fp8_full_size():
+    """The fp8 gate/up and down launches as bench.py times them at T = 32768
+    (8 local experts of about 1015 rows); every row is checked."""
+    _case(inputs.CONFIGS["c1p_fp8"])
+
+
+def test_c3_fp8_full_size_with_shared_expert():
+    """The fp8 launches as bench.py times them at T = 16384 with 32 local
+    experts and the shared expert over all tokens; every row is checked."""
+    _case(inputs.CONFIGS["c3_fp8"])
