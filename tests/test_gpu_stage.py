@@ -261,6 +261,46 @@ def test_streams_match_single_stream_bitwise():
         assert np.array_equal(a, b) and np.array_equal(a, c)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_three_stream_layout_matches_single_stream_bitwise(dtype):
+    """The three-stream layout bench.py times: dispatch, expert FFN and
+    combine of each micro-batch on three streams chained by events, six
+    micro-batches through three slots (a slot is reused once its last
+    combine has run), bit-identical to one stream with whole submissions."""
+    cfg = inputs.scaled(inputs.CONFIGS["c2"], d=512, f=256, n_micro=6, dtype=dtype,
+                        name="tri_" + dtype)
+    w = inputs.make_weights(cfg, "cuda")
+    mbs = inputs.make_microbatches(cfg, "cuda")
+    with ExpertStage(cfg, w, n_slots=3, max_tokens=cfg.max_tokens) as st:
+        ref, _, keep = gpu_run(st, mbs)
+        outs = []
+        for (x, xs, ids, wt, out, _) in keep:
+            o = torch.full_like(out, float("nan"))
+            outs.append((st.microbatch(x, ids, wt, o, xs), o))
+        D, G, R = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+        torch.cuda.synchronize()
+        slot_done = [None] * 3
+        for i, (m, _) in enumerate(outs):
+            k = i % 3
+            if slot_done[k] is not None:
+                D.wait_event(slot_done[k])
+            st.dispatch(k, m, D)
+            e1 = torch.cuda.Event()
+            e1.record(D)
+            G.wait_event(e1)
+            st.expert_ffn(k, G)
+            e2 = torch.cuda.Event()
+            e2.record(G)
+            R.wait_event(e2)
+            st.combine(k, R)
+            slot_done[k] = torch.cuda.Event()
+            slot_done[k].record(R)
+        st.sync()
+        torch.cuda.synchronize()
+    for i, ((_, o), r) in enumerate(zip(outs, ref)):
+        assert np.array_equal(bf16_bits(o), r), "micro-batch %d differs" % i
+
+
 # ---------------------------------------------------------------------------
 # Full-size configurations (every token and every routed row checked)
 # ---------------------------------------------------------------------------
